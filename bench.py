@@ -1,0 +1,210 @@
+"""Round-trip throughput of the constant-Q transform on one MI355X.
+
+One step = analysis T (packed FFT, routed band inverse FFTs) followed by
+synthesis S (band FFTs, owner overlap-add, packed inverse FFT) over one batch
+of synthetic audio resident in HBM. Default workload: 128 signals of 88,200
+samples at 22.05 kHz, 55 Hz..fs/2 at 36 bins per octave (the throughput
+stress workload). Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12          # MI355X HBM3E, bytes/s
+METRIC = "CQT analysis+synthesis round-trip audio samples/s and % HBM peak; round-trip SNR dB"
+
+
+class HipEvents:
+    """A few HIP events through the runtime's C API (timing only)."""
+
+    def __init__(self, n):
+        self.rt = ctypes.CDLL("libamdhip64.so")
+        self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            if self.rt.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev.append(e.value)
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.rt.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def close(self):
+        for e in self.ev:
+            self.rt.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_29119_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(workload, kernel):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel sources; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_hash") != kernel_source_hash():
+        return None
+    k = d.get("kernels", {}).get(kernel)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, x):
+    """The fp64 oracle's round trip on a bounded sample of the batch."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    lay = oracle.build_layout(*w.plan_args)
+    t0 = time.perf_counter()
+    oracle.synthesise(lay, oracle.analyse(lay, x[:1]))
+    t1 = time.perf_counter() - t0
+    k = int(max(1, min(x.shape[0], round(15.0 / max(t1, 1e-3)))))
+    t0 = time.perf_counter()
+    oracle.synthesise(lay, oracle.analyse(lay, x[:k]))
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": k * w.n_samples / dt, "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{k} of {x.shape[0]} signals, fp64 direct band DFTs, analysis+synthesis, {dt:.1f} s",
+            "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="stress")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stage-events", action="store_true",
+                    help="time the loop without per-kernel events (for profiler runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; a batch shards across GPUs with no "
+                          "communication, so --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    import workloads
+    import paper_2609_29119_amd as nc
+
+    w = workloads.WORKLOADS[args.workload]
+    if w.slice_len:
+        raise SystemExit("bench runs full-length workloads; use the sliced tests for the long one")
+    torch.cuda.init()
+    plan = nc.Plan(*w.plan_args, batch=w.batch)
+    x_np = workloads.signals(w)
+    x = torch.from_numpy(x_np).cuda()
+    c = torch.empty((w.batch, plan.n_coeffs), dtype=torch.complex64, device="cuda")
+    xr = torch.empty_like(x)
+    ws_a = plan.workspace(nc.OP_ANALYSE)
+    ws_s = plan.workspace(nc.OP_SYNTHESISE)
+
+    st_a = plan.stage_info(nc.OP_ANALYSE)
+    st_s = plan.stage_info(nc.OP_SYNTHESISE)
+    na, ns = len(st_a) + 1, len(st_s) + 1
+    K, W = args.steps, args.warmup
+    use_ev = not args.no_stage_events
+    ev = HipEvents(K * (na + ns)) if use_ev else None
+
+    def step(i=None):
+        if i is not None:
+            plan.set_stage_events(ev.ev[i * (na + ns): i * (na + ns) + na])
+        plan.analyse(x, out=c, ws=ws_a)
+        if i is not None:
+            plan.set_stage_events(ev.ev[i * (na + ns) + na: (i + 1) * (na + ns)])
+        plan.synthesise(c, out=xr, ws=ws_s)
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    t_start.record()
+    for i in range(K):
+        step(i if use_ev else None)
+    t_stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    plan.set_stage_events(None)
+    gpu_ms = t_start.elapsed_time(t_stop)
+    ms = max(gpu_ms, wall * 1e3) / K
+
+    # per-kernel durations from the stage events of the timed steps
+    stages = []
+    if use_ev:
+        names = [n for n, _ in st_a] + [n for n, _ in st_s]
+        algb = [b for _, b in st_a] + [b for _, b in st_s]
+        dur = np.zeros(len(names))
+        for i in range(K):
+            base = i * (na + ns)
+            for j in range(na - 1):
+                dur[j] += ev.elapsed_ms(ev.ev[base + j], ev.ev[base + j + 1])
+            for j in range(ns - 1):
+                dur[na - 1 + j] += ev.elapsed_ms(ev.ev[base + na + j], ev.ev[base + na + j + 1])
+        dur /= K
+        for n_, b_, d_ in zip(names, algb, dur):
+            stages.append({"kernel": n_, "ms": round(float(d_), 5), "alg_bytes": b_,
+                           "GBps": round(b_ / (d_ * 1e-3) / 1e9, 1)})
+        ev.close()
+
+    # accuracy of this run's round trip (GPU result against the input)
+    xr_np = xr.cpu().numpy().astype(np.float64)
+    x64 = x_np.astype(np.float64)
+    snr = 10 * np.log10(np.sum(x64 ** 2, axis=1) / np.sum((x64 - xr_np) ** 2, axis=1))
+
+    N, C, b = w.n_samples, plan.n_coeffs, w.batch
+    b_alg = (24.0 * N + 16.0 * C) * b              # method's algorithmic bytes per round trip
+    value = b * N / (ms * 1e-3)
+    out = {
+        "metric": METRIC, "value": value, "unit": "samples/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {b} x {N} samples @ {w.fs:g} Hz, {w.fmin:g} Hz..fs/2, "
+                               f"{w.bins_per_octave} bins/oct, analysis+synthesis round trip",
+                   "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": C},
+        "pct_hbm_peak": 100.0 * b_alg / (ms * 1e-3) / HBM_PEAK,
+        "alg_bytes_per_step": b_alg,
+        "snr_db_min": float(snr.min()),
+        "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_synthesise) / b,
+    }
+    if stages:
+        dom = max(stages, key=lambda s: s["ms"])
+        achieved = dom["alg_bytes"] / (dom["ms"] * 1e-3) / 1e9
+        out["roofline"] = {"bound": "hbm", "kernel": dom["kernel"], "achieved": round(achieved, 1),
+                           "peak": HBM_PEAK / 1e9, "unit": "GB/s", "frac": achieved / (HBM_PEAK / 1e9),
+                           "traffic": traffic_from_profiles(w.name, dom["kernel"])}
+        out["stages"] = stages
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, x_np)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,335 @@
+// HIP kernels of the packed constant-Q transform (Sec. 3, eqs. 5-10).
+//
+// Data layout in HBM (per signal, b signals back to back):
+//   x      N float32                          input / output signal
+//   Y      L complex64, row k1 of length L2  four-step intermediate
+//   Z      L complex64, natural order         packed spectrum Z = F_L P x
+//   c / W  C complex64, band offsets          coefficients / weighted band spectra
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "fft_lds.hpp"
+
+namespace nsg {
+
+constexpr int kWrSlots = 64;   // LDS complex slots reserved for a generic radix table
+
+// Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
+// caps each kernel at 256 VGPRs per lane.
+#define NSG_OCC __attribute__((amdgpu_waves_per_eu(2)))
+
+struct Tables {
+    const BandDev* bands;
+    const FftDesc* ffts;
+    const float2* tw;        // twiddle pool
+    const float2* omega;     // exp(-2 pi i k / N), k = 0..L
+    const int32_t* owner;    // first band covering bin k | count << 24, k = 0..L
+    const int32_t* bandbase; // off - k_lo per band
+    const float2* chirp;     // Bluestein exp(-i pi m^2 / M)
+    const float2* kern;      // Bluestein DFT_P(b) / P
+    const float2* tw4_hi;
+    const float2* tw4_lo;
+    const float* slicewin;
+    const int32_t* lists;    // band lists of the buckets
+};
+
+struct Pass {
+    int L1, L2;
+    int tile;                // columns (pass A) or rows (pass B) per workgroup
+    int ntile;
+    int ld;
+    int fft;                 // FftDesc index of the pass length
+    int split;               // four-step twiddle split
+    int L;
+};
+
+// Sliced input: slice s0 + sig of a signal x[n] with hop H, front pad H.
+struct SliceIn {
+    int enabled;
+    int s0;
+    long long n;
+    int H;
+};
+
+// Hardware dispatches workgroup b to XCD b mod 8; give each XCD a contiguous
+// range of logical ids so neighbouring tiles and bands share its L2.
+__device__ __forceinline__ int xcd_remap(int b, int G) {
+    const int x = b & 7, i = b >> 3;
+    const int q = G >> 3, r = G & 7;
+    return x * q + (x < r ? x : r) + i;
+}
+
+__device__ __forceinline__ float2 tw4(const Tables& T, int t, int split) {
+    return cmul(T.tw4_hi[t / split], T.tw4_lo[t % split]);
+}
+
+// -------------------------------------------------- packed FFT, pass A (columns)
+// Loads z_j = x_{2j} + i x_{2j+1} (eq. 5) for j = n1 L2 + n2 over a tile of
+// columns n2, runs the length-L1 column DFTs, multiplies by omega_L^{n2 k1} and
+// writes Y[k1 L2 + n2].
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
+                                              Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
+    extern __shared__ float2 lds[];
+    float2* wr = lds;
+    float2* buf = lds + kWrSlots;
+    const int G = p.ntile * batch;
+    const int lid = xcd_remap(blockIdx.x, G);
+    const int tile = lid % p.ntile, sig = lid / p.ntile;
+    const int n2a = tile * p.tile;
+    const int cols = min(p.tile, p.L2 - n2a);
+    const int tot = cols * p.L1;
+    if (!sl.enabled) {
+        const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
+        for (int e = threadIdx.x; e < tot; e += NT) {
+            const int c = e % cols, n1 = e / cols;
+            buf[c * p.ld + n1] = z[(long long)n1 * p.L2 + n2a + c];
+        }
+    } else {
+        // padded coordinate of sample 2j of slice s is s H + 2j; the signal
+        // starts at padded H
+        const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
+        for (int e = threadIdx.x; e < tot; e += NT) {
+            const int c = e % cols, n1 = e / cols;
+            const long long j = (long long)n1 * p.L2 + n2a + c;
+            const long long t = base + 2 * j;
+            const float v0 = (t >= 0 && t < sl.n) ? x[t] : 0.f;
+            const float v1 = (t + 1 >= 0 && t + 1 < sl.n) ? x[t + 1] : 0.f;
+            buf[c * p.ld + n1] = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
+        }
+    }
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr);
+    float2* Ys = Y + (long long)sig * p.L;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        const int c = e % cols, k1 = e / cols;
+        const int n2 = n2a + c;
+        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[c * p.ld + k1], tw4(T, n2 * k1, p.split));
+    }
+}
+
+// X_q = sum of the weighted band spectra W over the bands covering bin q.
+__device__ __forceinline__ float2 gather_bin(const Tables& T, const float2* __restrict__ Ws, int q) {
+    const int o = T.owner[q];
+    const int first = o & 0xFFFFFF, cnt = o >> 24;
+    float2 acc = make_float2(0.f, 0.f);
+    for (int i = 0; i < cnt; ++i) acc = cadd(acc, Ws[T.bandbase[first + i] + q]);
+    return acc;
+}
+
+// ------------------------------- inverse packed FFT, pass A, with overlap-add
+// For q = n1 L2 + n2 over a tile of columns: X_q and X_{L-q} are summed from
+// the bands that own those bins (no atomics: every packed bin is produced by
+// exactly one thread), made real at DC and Nyquist, and retangled into
+// Z_q = (1/2)[(1 + i conj(w_q)) X_q + (1 - i conj(w_q)) conj(X_{L-q})] (eq. 9).
+// The inverse DFT is taken as conj(F_L conj(Z)) / L.
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
+                                              Pass p, Tables T, int batch, long long C) {
+    extern __shared__ float2 lds[];
+    float2* wr = lds;
+    float2* buf = lds + kWrSlots;
+    const int G = p.ntile * batch;
+    const int lid = xcd_remap(blockIdx.x, G);
+    const int tile = lid % p.ntile, sig = lid / p.ntile;
+    const int n2a = tile * p.tile;
+    const int cols = min(p.tile, p.L2 - n2a);
+    const int tot = cols * p.L1;
+    const float2* Ws = W + (long long)sig * C;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        const int c = e % cols, n1 = e / cols;
+        const int q = n1 * p.L2 + n2a + c;
+        float2 xq = gather_bin(T, Ws, q);
+        float2 xm = gather_bin(T, Ws, p.L - q);
+        if (q == 0) { xq.y = 0.f; xm.y = 0.f; }
+        const float2 om = T.omega[q];                         // (cos, -sin)
+        const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w)
+        const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
+        const float2 zq = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
+        buf[c * p.ld + n1] = make_float2(0.5f * zq.x, -0.5f * zq.y);   // conj(Z_q)
+    }
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr);
+    float2* Ys = Y + (long long)sig * p.L;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        const int c = e % cols, k1 = e / cols;
+        const int n2 = n2a + c;
+        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[c * p.ld + k1], tw4(T, n2 * k1, p.split));
+    }
+}
+
+// ----------------------------------------------------- pass B (rows), both ways
+// Row k1 of Y (length L2) is transformed; output k = k1 + L1 k2.
+// INVERSE = false: Z[k] = result (natural order).
+// INVERSE = true : z_k = conj(result) / L, unpacked to x_{2k}, x_{2k+1} (P^{-1}).
+template <int NT, int EPT, bool INVERSE>
+__global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict__ Y, float2* __restrict__ out,
+                                               Pass p, Tables T, int batch, long long out_stride,
+                                               float inv_L) {
+    extern __shared__ float2 lds[];
+    float2* wr = lds;
+    float2* buf = lds + kWrSlots;
+    const int G = p.ntile * batch;
+    const int lid = xcd_remap(blockIdx.x, G);
+    const int tile = lid % p.ntile, sig = lid / p.ntile;
+    const int k1a = tile * p.tile;
+    const int rows = min(p.tile, p.L1 - k1a);
+    const int tot = rows * p.L2;
+    const float2* Ys = Y + (long long)sig * p.L + (long long)k1a * p.L2;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        const int r = e / p.L2, n2 = e - r * p.L2;
+        buf[r * p.ld + n2] = Ys[e];
+    }
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, rows, p.ld, T.ffts + p.fft, T.tw, wr);
+    float2* os = out + (long long)sig * out_stride;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        const int r = e % rows, k2 = e / rows;
+        const long long k = (long long)k1a + r + (long long)p.L1 * k2;
+        const float2 v = buf[r * p.ld + k2];
+        os[k] = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
+    }
+}
+
+// ------------------------------------------------------------ band analysis
+// One workgroup per (band, signal). For entry i of the band (bin k = k_lo + i)
+// the router (eq. 7) forms
+//   u = (1/2) w [(1 - i w_k) Z_{k mod L} + (1 + i w_k) conj(Z_{-k mod L})]
+// with w the band's weight at k (g for T, the S^dagger weight for S^dagger),
+// places conj(u) at slot (k - k_c) mod M in LDS, and the band's inverse DFT
+// (eq. 2) is conj(F_M conj(u)) / M. Bands whose length has a prime factor
+// above kGenericMaxRadix use Bluestein's algorithm: with ch_m = exp(-i pi m^2/M),
+// F_M v = ch * conj(F_P conj(F_P(ch v) * K)) where K = F_P(b)/P and b the
+// cyclic chirp exp(+i pi t^2/M), |t| < M.
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __restrict__ Z, float2* __restrict__ coef,
+                                                      const float* __restrict__ wt, Tables T, int list_off,
+                                                      int nbl, int batch, int L, long long C) {
+    extern __shared__ float2 lds[];
+    float2* wr = lds;
+    float2* buf = lds + kWrSlots;
+    const int G = nbl * batch;
+    const int lid = xcd_remap(blockIdx.x, G);
+    const int bi = lid % nbl, sig = lid / nbl;
+    const BandDev bd = T.bands[T.lists[list_off + bi]];
+    const FftDesc* fd = T.ffts + bd.fft;
+    const int M = bd.M;
+    const bool blu = bd.chirp >= 0;
+    const float2* Zs = Z + (long long)sig * L;
+    const float* w = wt + bd.off;
+    for (int i = threadIdx.x; i < M; i += NT) {
+        const int k = bd.k_lo + i;
+        const int a = (k == L) ? 0 : k;
+        const int bm = (a == 0) ? 0 : L - a;
+        const float2 za = Zs[a], zb = Zs[bm];
+        const float2 om = T.omega[k];                         // (cos, -sin)
+        const float2 pa = make_float2(1.f + om.y, -om.x);     // 1 - i w_k
+        const float2 pb = make_float2(1.f - om.y, om.x);      // 1 + i w_k
+        const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
+        const float hw = 0.5f * w[i];
+        float2 v = make_float2(hw * u2.x, -hw * u2.y);        // conj(u)
+        int slot = i + bd.rot;
+        if (slot >= M) slot -= M;
+        if (blu) v = cmul(v, T.chirp[bd.chirp + slot]);
+        buf[slot] = v;
+    }
+    if (blu)
+        for (int i = M + threadIdx.x; i < fd->n; i += NT) buf[i] = make_float2(0.f, 0.f);
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
+    float2* cs = coef + (long long)sig * C + bd.off;
+    if (!blu) {
+        for (int i = threadIdx.x; i < M; i += NT) {
+            const float2 v = buf[i];
+            cs[i] = make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+        }
+    } else {
+        const float2* K = T.kern + bd.kern;
+        for (int i = threadIdx.x; i < fd->n; i += NT) buf[i] = conjf2(cmul(buf[i], K[i]));
+        __syncthreads();
+        lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
+        const float2* ch = T.chirp + bd.chirp;
+        for (int i = threadIdx.x; i < M; i += NT) {
+            // c = conj(ch * conj(D)) / M = conj(ch) D / M
+            const float2 v = cmul(conjf2(ch[i]), buf[i]);
+            cs[i] = cscale(v, bd.inv_M);
+        }
+    }
+}
+
+// ----------------------------------------------------------- band synthesis
+// One workgroup per (band, signal): U = F_M c (eq. 10), then the weighted band
+// spectrum W[off + i] = w_i U[slot(k_lo + i)] in bin order (w = h for S, the
+// T^dagger weight for T^dagger). Overlapping bands are summed later by the
+// owner of each bin.
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __restrict__ coef, float2* __restrict__ W,
+                                                       const float* __restrict__ wt, Tables T, int list_off,
+                                                       int nbl, int batch, long long C) {
+    extern __shared__ float2 lds[];
+    float2* wr = lds;
+    float2* buf = lds + kWrSlots;
+    const int G = nbl * batch;
+    const int lid = xcd_remap(blockIdx.x, G);
+    const int bi = lid % nbl, sig = lid / nbl;
+    const BandDev bd = T.bands[T.lists[list_off + bi]];
+    const FftDesc* fd = T.ffts + bd.fft;
+    const int M = bd.M;
+    const bool blu = bd.chirp >= 0;
+    const float2* cs = coef + (long long)sig * C + bd.off;
+    const float2* ch = T.chirp + (blu ? bd.chirp : 0);
+    for (int i = threadIdx.x; i < M; i += NT) {
+        float2 v = cs[i];
+        if (blu) v = cmul(v, ch[i]);
+        buf[i] = v;
+    }
+    if (blu)
+        for (int i = M + threadIdx.x; i < fd->n; i += NT) buf[i] = make_float2(0.f, 0.f);
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
+    if (blu) {
+        const float2* K = T.kern + bd.kern;
+        for (int i = threadIdx.x; i < fd->n; i += NT) buf[i] = conjf2(cmul(buf[i], K[i]));
+        __syncthreads();
+        lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
+    }
+    float2* Ws = W + (long long)sig * C + bd.off;
+    const float* w = wt + bd.off;
+    for (int i = threadIdx.x; i < M; i += NT) {
+        int slot = i + bd.rot;
+        if (slot >= M) slot -= M;
+        float2 u = buf[slot];
+        if (blu) u = cmul(ch[slot], conjf2(u));
+        Ws[i] = cscale(u, w[i]);
+    }
+}
+
+// ------------------------------------------------------ sliced overlap-add
+// Output sample at padded position pp in [s0 H, (s0 + cnt) H) and inside the
+// signal: the slice sb = pp / H starting there and the slice sb - 1 ending
+// there contribute; slice s0 - 1 comes from the carry buffer (its upper half).
+// Also saves the upper half of the chunk's last slice for the next chunk.
+__global__ void k_ola(const float* __restrict__ y, const float* __restrict__ carry_in,
+                      float* __restrict__ carry_out, float* __restrict__ xo, int s0, int cnt, int Ns,
+                      long long n) {
+    const int H = Ns / 2;
+    const long long span = (long long)cnt * H;
+    for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < span;
+         e += (long long)gridDim.x * blockDim.x) {
+        const long long pp = (long long)s0 * H + e;
+        const long long t = pp - H;
+        if (t >= 0 && t < n) {
+            const int sb = (int)(pp / H);
+            const int lb = (int)(pp - (long long)sb * H);    // local index in slice sb, in [0, H)
+            float v = y[(long long)(sb - s0) * Ns + lb];
+            const int sa = sb - 1;
+            if (sa >= s0) v += y[(long long)(sa - s0) * Ns + lb + H];
+            else if (sa >= 0) v += carry_in[lb];
+            xo[t] = v;
+        }
+        if (e < H) carry_out[e] = y[(long long)(cnt - 1) * Ns + H + e];
+    }
+}
+
+}  // namespace nsg

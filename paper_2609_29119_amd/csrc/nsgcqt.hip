@@ -1,0 +1,516 @@
+// C ABI of the packed constant-Q transform: plan creation (host tables built in
+// fp64, uploaded once as fp32), and the enqueue-only compute calls.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/nsgcqt.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace nsg;
+
+namespace {
+
+thread_local std::string g_err;
+
+int set_err(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (expr);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            return set_err(NSGCQT_EDEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+}  // namespace
+
+struct nsgcqt_plan_s {
+    HostPlan h;
+    bool device = false;
+    void* dmem = nullptr;
+    int64_t dbytes = 0;
+    Tables T{};
+    const float* wA = nullptr;
+    const float* wS = nullptr;
+    const float* wT = nullptr;
+    const float* wSa = nullptr;
+    std::vector<hipEvent_t> events;
+    int ev_next = 0;
+};
+
+namespace {
+
+// ------------------------------------------------------------------ upload
+int upload(nsgcqt_plan_s* p) {
+    HostPlan& h = p->h;
+    struct Chunk { const void* src; int64_t bytes; int64_t off; };
+    std::vector<Chunk> ch;
+    int64_t total = 0;
+    auto add = [&](const void* src, int64_t bytes) {
+        ch.push_back({src, bytes, total});
+        total += align256(bytes > 0 ? bytes : 1);
+        return ch.size() - 1;
+    };
+    const size_t iBands = add(h.banddev.data(), h.banddev.size() * sizeof(BandDev));
+    const size_t iFfts = add(h.ffts.data(), h.ffts.size() * sizeof(FftDesc));
+    const size_t iTw = add(h.twpool.data(), h.twpool.size() * sizeof(float));
+    const size_t iOm = add(h.omega.data(), h.omega.size() * sizeof(float));
+    const size_t iOwn = add(h.owner.data(), h.owner.size() * sizeof(int32_t));
+    const size_t iBase = add(h.bandbase.data(), h.bandbase.size() * sizeof(int32_t));
+    const size_t iCh = add(h.chirp.data(), h.chirp.size() * sizeof(float));
+    const size_t iK = add(h.kern.data(), h.kern.size() * sizeof(float));
+    const size_t iHi = add(h.tw4_hi.data(), h.tw4_hi.size() * sizeof(float));
+    const size_t iLo = add(h.tw4_lo.data(), h.tw4_lo.size() * sizeof(float));
+    const size_t iWin = add(h.slicewin.data(), h.slicewin.size() * sizeof(float));
+    const size_t iList = add(h.bucket_lists.data(), h.bucket_lists.size() * sizeof(int32_t));
+    const size_t iWA = add(h.wA.data(), h.wA.size() * sizeof(float));
+    const size_t iWS = add(h.wS.data(), h.wS.size() * sizeof(float));
+    const size_t iWT = add(h.wT.data(), h.wT.size() * sizeof(float));
+    const size_t iWSa = add(h.wSa.data(), h.wSa.size() * sizeof(float));
+
+    char* d = nullptr;
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(&d), total);
+    if (e != hipSuccess) return set_err(NSGCQT_ENOMEM, std::string("hipMalloc of plan tables: ") + hipGetErrorString(e));
+    p->dmem = d;
+    p->dbytes = total;
+    for (const auto& c : ch)
+        if (c.bytes > 0) HIP_TRY(hipMemcpy(d + c.off, c.src, c.bytes, hipMemcpyHostToDevice));
+    auto at = [&](size_t i) { return static_cast<const void*>(d + ch[i].off); };
+    Tables& T = p->T;
+    T.bands = static_cast<const BandDev*>(at(iBands));
+    T.ffts = static_cast<const FftDesc*>(at(iFfts));
+    T.tw = static_cast<const float2*>(at(iTw));
+    T.omega = static_cast<const float2*>(at(iOm));
+    T.owner = static_cast<const int32_t*>(at(iOwn));
+    T.bandbase = static_cast<const int32_t*>(at(iBase));
+    T.chirp = static_cast<const float2*>(at(iCh));
+    T.kern = static_cast<const float2*>(at(iK));
+    T.tw4_hi = static_cast<const float2*>(at(iHi));
+    T.tw4_lo = static_cast<const float2*>(at(iLo));
+    T.slicewin = static_cast<const float*>(at(iWin));
+    T.lists = static_cast<const int32_t*>(at(iList));
+    p->wA = static_cast<const float*>(at(iWA));
+    p->wS = static_cast<const float*>(at(iWS));
+    p->wT = static_cast<const float*>(at(iWT));
+    p->wSa = static_cast<const float*>(at(iWSa));
+    p->device = true;
+    return NSGCQT_OK;
+}
+
+// ---------------------------------------------------------------- launches
+template <typename K>
+int launch_prep(K kernel, int lds_bytes) {
+    if (lds_bytes > 64 * 1024)
+        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes));
+    return NSGCQT_OK;
+}
+
+void record(nsgcqt_plan_s* p, hipStream_t s) {
+    if (p->ev_next < static_cast<int>(p->events.size())) hipEventRecord(p->events[p->ev_next++], s);
+}
+
+Pass pass_a(const HostPlan& h) {
+    Pass q{};
+    q.L1 = static_cast<int>(h.fs4.L1); q.L2 = static_cast<int>(h.fs4.L2);
+    q.tile = h.fs4.tile_a;
+    q.ntile = static_cast<int>((h.fs4.L2 + q.tile - 1) / q.tile);
+    q.ld = h.fs4.ld_a; q.fft = h.fs4.fft1;
+    q.split = static_cast<int>(h.fs4.split); q.L = static_cast<int>(h.L);
+    return q;
+}
+
+Pass pass_b(const HostPlan& h) {
+    Pass q = pass_a(h);
+    q.tile = h.fs4.tile_b;
+    q.ntile = static_cast<int>((h.fs4.L1 + q.tile - 1) / q.tile);
+    q.ld = h.fs4.ld_b; q.fft = h.fs4.fft2;
+    return q;
+}
+
+int lds_pass(const Pass& q) { return (kWrSlots + q.tile * q.ld) * static_cast<int>(sizeof(float2)); }
+
+#define DISPATCH_NT(nt, KERNEL, ...)                                                         \
+    switch (nt) {                                                                            \
+        case 256: { auto k_ = KERNEL<256, 8 __VA_ARGS__>; if (int r_ = launch(k_)) return r_; break; } \
+        case 512: { auto k_ = KERNEL<512, 8 __VA_ARGS__>; if (int r_ = launch(k_)) return r_; break; } \
+        default: { auto k_ = KERNEL<1024, 8 __VA_ARGS__>; if (int r_ = launch(k_)) return r_; break; } \
+    }
+
+int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl, long long sig_stride,
+              hipStream_t s) {
+    const Pass q = pass_a(p->h);
+    const int lds = lds_pass(q);
+    auto launch = [&](auto k) -> int {
+        if (int r = launch_prep(k, lds)) return r;
+        hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch,
+                           sig_stride);
+        HIP_TRY(hipGetLastError());
+        record(p, s);
+        return NSGCQT_OK;
+    };
+    DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a)
+    return NSGCQT_OK;
+}
+
+int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream_t s) {
+    const Pass q = pass_a(p->h);
+    const int lds = lds_pass(q);
+    auto launch = [&](auto k) -> int {
+        if (int r = launch_prep(k, lds)) return r;
+        hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, W, Y, q, p->T, batch,
+                           static_cast<long long>(p->h.C));
+        HIP_TRY(hipGetLastError());
+        record(p, s);
+        return NSGCQT_OK;
+    };
+    DISPATCH_NT(p->h.fs4.nt_a, k_inv_a)
+    return NSGCQT_OK;
+}
+
+template <bool INV>
+int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long long out_stride, hipStream_t s) {
+    const Pass q = pass_b(p->h);
+    const int lds = lds_pass(q);
+    const float inv_L = static_cast<float>(1.0 / static_cast<double>(p->h.L));
+    auto launch = [&](auto k) -> int {
+        if (int r = launch_prep(k, lds)) return r;
+        hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_b), lds, s, Y, out, q, p->T, batch,
+                           out_stride, inv_L);
+        HIP_TRY(hipGetLastError());
+        record(p, s);
+        return NSGCQT_OK;
+    };
+    DISPATCH_NT(p->h.fs4.nt_b, k_pass_b, , INV)
+    return NSGCQT_OK;
+}
+
+int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float* wt, int batch,
+              hipStream_t s) {
+    const HostPlan& h = p->h;
+    for (const auto& bk : h.buckets) {
+        const int nbl = static_cast<int>(bk.bands.size());
+        const int lds = (kWrSlots + bk.max_work) * static_cast<int>(sizeof(float2));
+        const dim3 grid(nbl * batch), block(bk.nt);
+        auto go = [&](auto ka, auto ks) -> int {
+            if (analysis) {
+                if (int r = launch_prep(ka, lds)) return r;
+                hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, wt, p->T, bk.list_off, nbl, batch,
+                                   static_cast<int>(h.L), static_cast<long long>(h.C));
+            } else {
+                if (int r = launch_prep(ks, lds)) return r;
+                hipLaunchKernelGGL(ks, grid, block, lds, s, in, out, wt, p->T, bk.list_off, nbl, batch,
+                                   static_cast<long long>(h.C));
+            }
+            HIP_TRY(hipGetLastError());
+            record(p, s);
+            return NSGCQT_OK;
+        };
+        int r = NSGCQT_OK;
+        if (bk.nt == 64) r = go(k_band_analysis<64, 8>, k_band_synthesis<64, 8>);
+        else if (bk.nt == 256) r = go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
+        else if (bk.ept == 8) r = go(k_band_analysis<1024, 8>, k_band_synthesis<1024, 8>);
+        else r = go(k_band_analysis<1024, 16>, k_band_synthesis<1024, 16>);
+        if (r) return r;
+    }
+    return NSGCQT_OK;
+}
+
+// Analysis chain (T, or S^dagger with its weights) for `batch` signals or slices.
+int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float* wt, int batch, SliceIn sl,
+                  char* ws, hipStream_t s) {
+    const HostPlan& h = p->h;
+    float2* Y = reinterpret_cast<float2*>(ws);
+    float2* Z = reinterpret_cast<float2*>(ws + align256(8 * h.L * batch));
+    if (int r = run_fwd_a(p, x, Y, batch, sl, static_cast<long long>(h.N), s)) return r;
+    if (int r = run_pass_b<false>(p, Y, Z, batch, static_cast<long long>(h.L), s)) return r;
+    return run_bands(p, true, Z, coeffs, wt, batch, s);
+}
+
+// Synthesis chain (S, or T^dagger with its weights); output is [batch][N] f32.
+int chain_synthesise(nsgcqt_plan_s* p, const float2* coeffs, float* xo, const float* wt, int batch, char* ws,
+                     hipStream_t s) {
+    const HostPlan& h = p->h;
+    float2* W = reinterpret_cast<float2*>(ws);
+    float2* Y = reinterpret_cast<float2*>(ws + align256(8 * h.C * batch));
+    if (int r = run_bands(p, false, coeffs, W, wt, batch, s)) return r;
+    if (int r = run_inv_a(p, W, Y, batch, s)) return r;
+    return run_pass_b<true>(p, Y, reinterpret_cast<float2*>(xo), batch, static_cast<long long>(h.L), s);
+}
+
+int check_call(nsgcqt_plan_s* p, const void* in, const void* out, const void* ws, size_t ws_bytes,
+               int64_t need, bool want_sliced) {
+    if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
+    if (!in || !out) return set_err(NSGCQT_EINVAL, "input or output pointer is NULL");
+    if (p->h.sliced != want_sliced)
+        return set_err(NSGCQT_EINVAL, want_sliced ? "plan is not a sliced plan" : "plan is a sliced plan");
+    if (static_cast<int64_t>(ws_bytes) < need)
+        return set_err(NSGCQT_EWORKSPACE, "workspace of " + std::to_string(ws_bytes) + " bytes, " +
+                                              std::to_string(need) + " required");
+    if (need > 0 && !ws) return set_err(NSGCQT_EINVAL, "workspace pointer is NULL");
+    if (!p->device) return set_err(NSGCQT_EINVAL, "host-only plan has no device tables");
+    return NSGCQT_OK;
+}
+
+int create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t n, int batch, bool sliced,
+           bool device) {
+    if (!out) return set_err(NSGCQT_EINVAL, "out is NULL");
+    *out = nullptr;
+    nsgcqt_plan_s* p = new (std::nothrow) nsgcqt_plan_s();
+    if (!p) return set_err(NSGCQT_ENOMEM, "host allocation failed");
+    std::string err;
+    int r;
+    try {
+        r = build_host_plan(p->h, fs, fmin, fmax, bpo, n, batch, sliced, err);
+    } catch (const std::bad_alloc&) {
+        r = NSGCQT_ENOMEM;
+        err = "host allocation failed while building the plan";
+    } catch (const std::exception& ex) {
+        r = NSGCQT_EINVAL;
+        err = ex.what();
+    }
+    if (r != NSGCQT_OK) {
+        delete p;
+        return set_err(r, err);
+    }
+    if (device) {
+        r = upload(p);
+        if (r != NSGCQT_OK) {
+            if (p->dmem) hipFree(p->dmem);
+            delete p;
+            return r;
+        }
+    }
+    *out = p;
+    return NSGCQT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int nsgcqt_plan_create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t n, int batch) {
+    return create(out, fs, fmin, fmax, bpo, n, batch, false, true);
+}
+
+int nsgcqt_plan_create_host(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t n,
+                            int batch) {
+    return create(out, fs, fmin, fmax, bpo, n, batch, false, false);
+}
+
+int nsgcqt_sliced_plan_create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t slice_len,
+                              int spc) {
+    return create(out, fs, fmin, fmax, bpo, slice_len, spc, true, true);
+}
+
+int nsgcqt_sliced_plan_create_host(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo,
+                                   int64_t slice_len, int spc) {
+    return create(out, fs, fmin, fmax, bpo, slice_len, spc, true, false);
+}
+
+int nsgcqt_plan_destroy(nsgcqt_plan p) {
+    if (!p) return NSGCQT_OK;
+    int r = NSGCQT_OK;
+    if (p->dmem) {
+        hipError_t e = hipFree(p->dmem);
+        if (e != hipSuccess) r = set_err(NSGCQT_EDEVICE, std::string("hipFree: ") + hipGetErrorString(e));
+    }
+    delete p;
+    return r;
+}
+
+int nsgcqt_plan_info(nsgcqt_plan p, nsgcqt_info* o) {
+    if (!p || !o) return set_err(NSGCQT_EINVAL, "NULL argument");
+    const HostPlan& h = p->h;
+    std::memset(o, 0, sizeof(*o));
+    o->n_bands = static_cast<int64_t>(h.bands.size());
+    o->batch = h.batch;
+    o->n_samples = h.N;
+    o->packed_len = h.L;
+    o->total_coeffs = h.C;
+    o->max_band_len = h.maxM;
+    o->max_fanout = h.max_fanout;
+    o->max_overlap = h.max_overlap;
+    o->sliced = h.sliced ? 1 : 0;
+    o->ws_analyse = h.ws_an;
+    o->ws_synthesise = h.ws_syn;
+    o->ws_adjoint_analysis = h.ws_syn;
+    o->ws_adjoint_synthesis = h.ws_an;
+    o->table_bytes = p->dbytes;
+    o->device_tables = p->device ? 1 : 0;
+    return NSGCQT_OK;
+}
+
+int nsgcqt_band_info(nsgcqt_plan p, int band, nsgcqt_band* o) {
+    if (!p || !o) return set_err(NSGCQT_EINVAL, "NULL argument");
+    if (band < 0 || band >= static_cast<int>(p->h.bands.size()))
+        return set_err(NSGCQT_EINVAL, "band index out of range");
+    const HostBand& b = p->h.bands[band];
+    o->kind = b.kind;
+    o->k_lo = b.k_lo;
+    o->k_hi = b.k_hi;
+    o->k_centre = b.k_c;
+    o->length = b.M;
+    o->offset = b.off;
+    o->centre_hz = b.f;
+    o->xi = b.xi;
+    o->beta = b.beta;
+    return NSGCQT_OK;
+}
+
+int nsgcqt_plan_weights(nsgcqt_plan p, int which, float* dst, size_t bytes) {
+    if (!p || !dst) return set_err(NSGCQT_EINVAL, "NULL argument");
+    const std::vector<float>* v = nullptr;
+    switch (which) {
+        case 0: v = &p->h.wA; break;
+        case 1: v = &p->h.wS; break;
+        case 2: v = &p->h.wT; break;
+        case 3: v = &p->h.wSa; break;
+        default: return set_err(NSGCQT_EINVAL, "weight table index must be 0..3");
+    }
+    if (bytes < v->size() * sizeof(float)) return set_err(NSGCQT_EINVAL, "destination too small");
+    std::memcpy(dst, v->data(), v->size() * sizeof(float));
+    return NSGCQT_OK;
+}
+
+int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_t ws_bytes, void* stream) {
+    if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, false)) return r;
+    p->ev_next = 0;
+    record(p, static_cast<hipStream_t>(stream));
+    return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->wA, p->h.batch, SliceIn{0, 0, 0, 0},
+                         static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+}
+
+int nsgcqt_synthesise(nsgcqt_plan p, const float* coeffs, float* xo, void* ws, size_t ws_bytes, void* stream) {
+    if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, false)) return r;
+    p->ev_next = 0;
+    record(p, static_cast<hipStream_t>(stream));
+    return chain_synthesise(p, reinterpret_cast<const float2*>(coeffs), xo, p->wS, p->h.batch,
+                            static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+}
+
+int nsgcqt_adjoint(nsgcqt_plan p, int op, const float* in, float* out, void* ws, size_t ws_bytes, void* stream) {
+    if (op != NSGCQT_OP_ADJ_ANALYSIS && op != NSGCQT_OP_ADJ_SYNTHESIS)
+        return set_err(NSGCQT_EINVAL, "op must be NSGCQT_OP_ADJ_ANALYSIS or NSGCQT_OP_ADJ_SYNTHESIS");
+    const bool ta = op == NSGCQT_OP_ADJ_ANALYSIS;
+    if (int r = check_call(p, in, out, ws, ws_bytes, p ? (ta ? p->h.ws_syn : p->h.ws_an) : 0, false)) return r;
+    p->ev_next = 0;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    record(p, s);
+    if (ta)
+        return chain_synthesise(p, reinterpret_cast<const float2*>(in), out, p->wT, p->h.batch,
+                                static_cast<char*>(ws), s);
+    return chain_analyse(p, in, reinterpret_cast<float2*>(out), p->wSa, p->h.batch, SliceIn{0, 0, 0, 0},
+                         static_cast<char*>(ws), s);
+}
+
+int64_t nsgcqt_sliced_count(nsgcqt_plan p, int64_t n) {
+    if (!p || !p->h.sliced) return set_err(NSGCQT_EINVAL, "not a sliced plan");
+    if (n < 0) return set_err(NSGCQT_EINVAL, "negative length");
+    const int64_t H = p->h.N / 2;
+    return (n + H - 1) / H + 1;
+}
+
+int nsgcqt_sliced_analyse(nsgcqt_plan p, const float* x, int64_t n, float* coeffs, void* ws, size_t ws_bytes,
+                          void* stream) {
+    if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, true)) return r;
+    if (n < 1) return set_err(NSGCQT_EINVAL, "signal length must be >= 1");
+    const HostPlan& h = p->h;
+    const int64_t J = nsgcqt_sliced_count(p, n);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    p->ev_next = 0;
+    record(p, s);
+    for (int64_t s0 = 0; s0 < J; s0 += h.spc) {
+        const int cnt = static_cast<int>(std::min<int64_t>(h.spc, J - s0));
+        SliceIn sl{1, static_cast<int>(s0), static_cast<long long>(n), static_cast<int>(h.N / 2)};
+        float2* c = reinterpret_cast<float2*>(coeffs) + s0 * h.C;
+        if (int r = chain_analyse(p, x, c, p->wA, cnt, sl, static_cast<char*>(ws), s)) return r;
+    }
+    return NSGCQT_OK;
+}
+
+int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, float* xo, void* ws,
+                             size_t ws_bytes, void* stream) {
+    if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, true)) return r;
+    if (n < 1) return set_err(NSGCQT_EINVAL, "signal length must be >= 1");
+    const HostPlan& h = p->h;
+    const int64_t J = nsgcqt_sliced_count(p, n);
+    const int64_t H = h.N / 2;
+    char* w = static_cast<char*>(ws);
+    const int64_t chain_bytes = align256(8 * h.C * h.spc) + align256(8 * h.L * h.spc);
+    float* y = reinterpret_cast<float*>(w + chain_bytes);
+    float* carry[2] = {reinterpret_cast<float*>(w + chain_bytes + align256(4 * h.N * h.spc)),
+                       reinterpret_cast<float*>(w + chain_bytes + align256(4 * h.N * h.spc) + align256(4 * H))};
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    p->ev_next = 0;
+    record(p, s);
+    int flip = 0;
+    for (int64_t s0 = 0; s0 < J; s0 += h.spc) {
+        const int cnt = static_cast<int>(std::min<int64_t>(h.spc, J - s0));
+        const float2* c = reinterpret_cast<const float2*>(coeffs) + s0 * h.C;
+        if (int r = chain_synthesise(p, c, y, p->wS, cnt, w, s)) return r;
+        const int64_t span = static_cast<int64_t>(cnt) * H;
+        const int blocks = static_cast<int>(std::min<int64_t>((span + 255) / 256, 8192));
+        hipLaunchKernelGGL(k_ola, dim3(blocks), dim3(256), 0, s, y, carry[flip], carry[flip ^ 1], xo,
+                           static_cast<int>(s0), cnt, static_cast<int>(h.N), static_cast<long long>(n));
+        HIP_TRY(hipGetLastError());
+        record(p, s);
+        flip ^= 1;
+    }
+    return NSGCQT_OK;
+}
+
+int nsgcqt_set_stage_events(nsgcqt_plan p, void* const* events, int n_events) {
+    if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
+    p->events.clear();
+    p->ev_next = 0;
+    if (events && n_events > 0)
+        for (int i = 0; i < n_events; ++i) p->events.push_back(static_cast<hipEvent_t>(events[i]));
+    return NSGCQT_OK;
+}
+
+int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, double* alg_bytes) {
+    if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
+    if (p->h.sliced) return set_err(NSGCQT_EUNSUPPORTED, "stage info is reported for non-sliced plans");
+    if (op < 0 || op > 3) return set_err(NSGCQT_EINVAL, "unknown op");
+    const HostPlan& h = p->h;
+    const double b = h.batch, L = static_cast<double>(h.L), C = static_cast<double>(h.C);
+    struct St { std::string name; double bytes; };
+    std::vector<St> st;
+    const bool an = (op == NSGCQT_OP_ANALYSE || op == NSGCQT_OP_ADJ_SYNTHESIS);
+    if (an) {
+        st.push_back({"fft_fwd_a", 16.0 * L * b});
+        st.push_back({"fft_fwd_b", 16.0 * L * b});
+        for (const auto& bk : h.buckets) {
+            const double cb = static_cast<double>(bk.coeffs);
+            st.push_back({"band_analysis_" + std::to_string(bk.nt), (cb / C * 8.0 * L + 8.0 * cb) * b});
+        }
+    } else {
+        for (const auto& bk : h.buckets)
+            st.push_back({"band_synthesis_" + std::to_string(bk.nt), 16.0 * static_cast<double>(bk.coeffs) * b});
+        st.push_back({"fft_inv_a_overlap_add", (8.0 * C + 8.0 * L) * b});
+        st.push_back({"fft_inv_b", 16.0 * L * b});
+    }
+    if (i >= 0 && i < static_cast<int>(st.size())) {
+        if (name && cap) {
+            std::strncpy(name, st[i].name.c_str(), cap - 1);
+            name[cap - 1] = 0;
+        }
+        if (alg_bytes) *alg_bytes = st[i].bytes;
+    }
+    return static_cast<int>(st.size());
+}
+
+const char* nsgcqt_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,419 @@
+// Host plan builder: band layout, windows, dual windows, routing weights,
+// ownership of bins for the atomics-free overlap-add, FFT plans, twiddles and
+// Bluestein tables. All values are computed in fp64 and rounded once to fp32.
+#include "plan.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <complex>
+#include <map>
+
+#include "../../include/nsgcqt.h"
+
+namespace nsg {
+
+namespace {
+
+using cd = std::complex<double>;
+constexpr double kPi = 3.14159265358979323846264338327950288;
+
+int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+// exp(-2 pi i t / n) with t reduced modulo n first.
+cd root(int64_t t, int64_t n) {
+    t %= n;
+    if (t < 0) t += n;
+    const double ang = 2.0 * kPi * static_cast<double>(t) / static_cast<double>(n);
+    return cd(std::cos(ang), -std::sin(ang));
+}
+
+int smallest_prime_factor(int64_t n) {
+    if (n % 2 == 0) return 2;
+    for (int64_t p = 3; p * p <= n; p += 2)
+        if (n % p == 0) return static_cast<int>(p);
+    return static_cast<int>(n);
+}
+
+// Forward DFT (eq. 1) of a 7-smooth length in fp64, recursive decimation in
+// time. Used only at plan time for the Bluestein kernels.
+void host_dft(std::vector<cd>& x) {
+    const int64_t n = static_cast<int64_t>(x.size());
+    if (n <= 1) return;
+    const int p = smallest_prime_factor(n);
+    const int64_t m = n / p;
+    std::vector<std::vector<cd>> sub(p, std::vector<cd>(m));
+    for (int64_t j = 0; j < m; ++j)
+        for (int r = 0; r < p; ++r) sub[r][j] = x[j * p + r];
+    for (int r = 0; r < p; ++r) host_dft(sub[r]);
+    for (int64_t k = 0; k < n; ++k) {
+        cd acc = 0.0;
+        for (int r = 0; r < p; ++r) acc += sub[r][k % m] * root(static_cast<int64_t>(r) * k, n);
+        x[k] = acc;
+    }
+}
+
+int64_t smooth7_at_least(int64_t target) {
+    int64_t best = INT64_MAX;
+    for (int64_t a = 1; a < 4 * target; a *= 2)
+        for (int64_t b = a; b < 4 * target; b *= 3)
+            for (int64_t c = b; c < 4 * target; c *= 5)
+                for (int64_t d = c; d < 4 * target; d *= 7)
+                    if (d >= target && d < best) best = d;
+    return best;
+}
+
+void push_c(std::vector<float>& v, cd z) {
+    v.push_back(static_cast<float>(z.real()));
+    v.push_back(static_cast<float>(z.imag()));
+}
+
+}  // namespace
+
+bool factor_radices(int64_t n, std::vector<int>& out) {
+    out.clear();
+    if (n < 1) return false;
+    int64_t m = n;
+    int e2 = 0;
+    while (m % 2 == 0) { m /= 2; ++e2; }
+    // powers of two as radix-8 stages, with a radix-4 pair or a single 4 or 2
+    // for the remainder
+    if (e2 % 3 == 1 && e2 >= 4) { out.push_back(4); out.push_back(4); e2 -= 4; }
+    while (e2 >= 3) { out.push_back(8); e2 -= 3; }
+    if (e2 == 2) out.push_back(4);
+    if (e2 == 1) out.push_back(2);
+    for (int p : {3, 5, 7})
+        while (m % p == 0) { out.push_back(p); m /= p; }
+    for (int64_t p = 11; m > 1; p += 2) {
+        if (p * p > m) p = m;   // m is prime now
+        while (m % p == 0) {
+            if (p > kGenericMaxRadix) return false;
+            out.push_back(static_cast<int>(p));
+            m /= p;
+        }
+    }
+    return static_cast<int>(out.size()) <= kMaxStages;
+}
+
+namespace {
+
+struct FftRegistry {
+    HostPlan& p;
+    std::map<int64_t, int> index;
+    explicit FftRegistry(HostPlan& plan) : p(plan) {}
+
+    // Index of the FftDesc for length n, creating it (and its twiddles) on
+    // first use; -1 if n does not factor into supported radices.
+    int get(int64_t n) {
+        auto it = index.find(n);
+        if (it != index.end()) return it->second;
+        std::vector<int> rad;
+        if (!factor_radices(n, rad)) return -1;
+        FftDesc d{};
+        d.n = static_cast<int32_t>(n);
+        d.nstages = static_cast<int32_t>(rad.size());
+        d.tw = static_cast<int32_t>(p.twpool.size() / 2);
+        d.max_generic = 0;
+        for (size_t s = 0; s < rad.size(); ++s) {
+            d.radix[s] = static_cast<int16_t>(rad[s]);
+            if (rad[s] > 8) d.max_generic = std::max(d.max_generic, rad[s]);
+        }
+        for (int64_t t = 0; t < n; ++t) push_c(p.twpool, root(t, n));
+        p.ffts.push_back(d);
+        const int id = static_cast<int>(p.ffts.size()) - 1;
+        index[n] = id;
+        return id;
+    }
+};
+
+int fail(std::string& err, int code, const std::string& msg) {
+    err = msg;
+    return code;
+}
+
+}  // namespace
+
+int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
+                    int64_t N, int batch, bool sliced, std::string& err) {
+    if (!(N >= 4) || (N % 2) != 0)
+        return fail(err, NSGCQT_EINVAL, "n_samples must be even and >= 4");
+    if (!(fs > 0.0)) return fail(err, NSGCQT_EINVAL, "fs must be > 0");
+    if (!(fmin > 0.0) || !(fmin < fs / 2.0))
+        return fail(err, NSGCQT_EINVAL, "fmin must satisfy 0 < fmin < fs/2");
+    if (!(fmax >= fmin)) return fail(err, NSGCQT_EINVAL, "fmax must be >= fmin");
+    if (B < 1) return fail(err, NSGCQT_EINVAL, "bins_per_octave must be >= 1");
+    if (batch < 1) return fail(err, NSGCQT_EINVAL, "batch must be >= 1");
+    if (sliced && (N % 8) != 0)
+        return fail(err, NSGCQT_EINVAL, "slice length must be a multiple of 8");
+    if (N > (int64_t(1) << 30))
+        return fail(err, NSGCQT_EUNSUPPORTED, "n_samples above 2^30");
+
+    p.fs = fs; p.fmin = fmin; p.fmax = fmax; p.bpo = B;
+    p.N = N; p.L = N / 2; p.batch = batch; p.sliced = sliced;
+    p.spc = sliced ? batch : 0;
+    const int64_t half = N / 2, L = p.L;
+
+    // ---- layout: geometric centres, Hann windows, DC and Nyquist sidebands
+    const double Q = 1.0 / (std::pow(2.0, 1.0 / B) - 1.0);
+    std::vector<double> fc, xis, betas;
+    for (int j = 0;; ++j) {
+        const double f = fmin * std::pow(2.0, static_cast<double>(j) / B);
+        if (!(f <= fmax * (1.0 + 1e-12) && f < fs / 2.0)) break;
+        fc.push_back(f);
+        xis.push_back(f * static_cast<double>(N) / fs);
+        betas.push_back((f / Q) * static_cast<double>(N) / fs);
+    }
+    p.bands.clear();
+    {
+        const double xi0 = xis.front(), b0 = betas.front();
+        HostBand b{};
+        b.kind = 0; b.k_lo = 0; b.k_hi = static_cast<int64_t>(std::ceil(xi0)) - 1; b.k_c = 0;
+        b.f = 0.0; b.xi = xi0; b.beta = b0;
+        for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+            const double kd = static_cast<double>(k);
+            const double s = std::sin(kPi * (xi0 - kd) / (2.0 * b0));
+            b.g.push_back(kd <= xi0 - b0 ? 1.0 : s * s);
+        }
+        p.bands.push_back(std::move(b));
+    }
+    for (size_t j = 0; j < fc.size(); ++j) {
+        const double xi = xis[j], beta = betas[j];
+        const int64_t k_lo = std::max<int64_t>(0, static_cast<int64_t>(std::floor(xi - beta)) + 1);
+        const int64_t k_hi = std::min<int64_t>(half, static_cast<int64_t>(std::ceil(xi + beta)) - 1);
+        if (k_hi < k_lo) continue;
+        HostBand b{};
+        b.kind = 1; b.k_lo = k_lo; b.k_hi = k_hi;
+        b.k_c = static_cast<int64_t>(std::floor(xi + 0.5));
+        b.f = fc[j]; b.xi = xi; b.beta = beta;
+        for (int64_t k = k_lo; k <= k_hi; ++k) {
+            const double c = std::cos(kPi * (static_cast<double>(k) - xi) / (2.0 * beta));
+            b.g.push_back(c * c);
+        }
+        p.bands.push_back(std::move(b));
+    }
+    {
+        const double xl = xis.back(), bl = betas.back();
+        HostBand b{};
+        b.kind = 2; b.k_lo = static_cast<int64_t>(std::floor(xl)) + 1; b.k_hi = half; b.k_c = half;
+        b.f = fs / 2.0; b.xi = xl; b.beta = bl;
+        for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+            const double kd = static_cast<double>(k);
+            const double s = std::sin(kPi * (kd - xl) / (2.0 * bl));
+            b.g.push_back(kd >= xl + bl ? 1.0 : s * s);
+        }
+        p.bands.push_back(std::move(b));
+    }
+
+    // ---- aggregate weight and dual windows (Sec. 2)
+    p.a.assign(half + 1, 0.0);
+    int64_t off = 0;
+    p.maxM = 0;
+    for (auto& b : p.bands) {
+        b.M = b.k_hi - b.k_lo + 1;
+        b.off = off;
+        off += b.M;
+        p.maxM = std::max(p.maxM, b.M);
+        for (int64_t i = 0; i < b.M; ++i) p.a[b.k_lo + i] += static_cast<double>(b.M) * b.g[i] * b.g[i];
+    }
+    p.C = off;
+    for (int64_t k = 0; k <= half; ++k)
+        if (!(p.a[k] > 0.0)) return fail(err, NSGCQT_EINVAL, "layout leaves bin " + std::to_string(k) + " uncovered (a_k = 0)");
+    if (p.C * static_cast<int64_t>(batch) * 8 > (int64_t(1) << 46))
+        return fail(err, NSGCQT_EUNSUPPORTED, "coefficient array too large");
+    for (auto& b : p.bands) {
+        b.h.resize(b.M);
+        for (int64_t i = 0; i < b.M; ++i) b.h[i] = static_cast<double>(b.M) * b.g[i] / p.a[b.k_lo + i];
+    }
+
+    // ---- per-coefficient weight tables in bin order (Sec. 3, eq. 7 and Sec. 3.2)
+    p.wA.resize(p.C); p.wS.resize(p.C); p.wT.resize(p.C); p.wSa.resize(p.C);
+    for (auto& b : p.bands)
+        for (int64_t i = 0; i < b.M; ++i) {
+            const int64_t k = b.k_lo + i;
+            const double d = (k == 0 || k == half) ? 1.0 : 2.0;
+            const double M = static_cast<double>(b.M);
+            p.wA[b.off + i] = static_cast<float>(b.g[i]);
+            p.wS[b.off + i] = static_cast<float>(b.h[i]);
+            p.wT[b.off + i] = static_cast<float>(static_cast<double>(N) / (d * M) * b.g[i]);
+            p.wSa[b.off + i] = static_cast<float>(M * d / static_cast<double>(N) * b.h[i]);
+        }
+
+    // ---- bin ownership for the overlap-add and fan-out statistics
+    p.owner.assign(half + 1, -1);
+    std::vector<int32_t> cnt(half + 1, 0);
+    for (size_t l = 0; l < p.bands.size(); ++l) {
+        const auto& b = p.bands[l];
+        for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+            if (p.owner[k] < 0) p.owner[k] = static_cast<int32_t>(l);
+            else if (p.owner[k] + cnt[k] != static_cast<int32_t>(l))
+                return fail(err, NSGCQT_EUNSUPPORTED, "bands covering a bin are not consecutive");
+            ++cnt[k];
+        }
+    }
+    p.max_overlap = 0;
+    for (int64_t k = 0; k <= half; ++k) {
+        if (cnt[k] > 127 || p.bands.size() >= (1u << 24))
+            return fail(err, NSGCQT_EUNSUPPORTED, "too many bands per bin");
+        p.max_overlap = std::max<int64_t>(p.max_overlap, cnt[k]);
+        p.owner[k] |= cnt[k] << 24;
+    }
+    {
+        std::vector<int32_t> fan(L / 2 + 1, 0);
+        for (const auto& b : p.bands)
+            for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+                const int64_t q = k % L, r = (L - q) % L;
+                ++fan[std::min(q, r)];
+            }
+        p.max_fanout = *std::max_element(fan.begin(), fan.end());
+    }
+    p.bandbase.resize(p.bands.size());
+    for (size_t l = 0; l < p.bands.size(); ++l)
+        p.bandbase[l] = static_cast<int32_t>(p.bands[l].off - p.bands[l].k_lo);
+
+    // ---- omega_k = exp(-2 pi i k / N) for the untangle (eq. 6) and retangle (eq. 9)
+    p.omega.clear();
+    for (int64_t k = 0; k <= L; ++k) push_c(p.omega, root(k, N));
+
+    // ---- packed FFT: four-step split L = L1 * L2
+    p.ffts.clear(); p.twpool.clear();
+    FftRegistry reg(p);
+    {
+        int64_t best = -1;
+        for (int64_t d = 1; d * d <= L; ++d) {
+            if (L % d) continue;
+            std::vector<int> r1, r2;
+            if (factor_radices(d, r1) && factor_radices(L / d, r2)) best = d;
+        }
+        if (best < 0)
+            return fail(err, NSGCQT_EUNSUPPORTED,
+                        "packed length L = " + std::to_string(L) + " has a prime factor above " +
+                            std::to_string(kGenericMaxRadix));
+        auto& f = p.fs4;
+        f.L1 = best; f.L2 = L / best;
+        if (f.L2 > 8192) return fail(err, NSGCQT_EUNSUPPORTED, "packed length too large for the two-pass FFT");
+        f.fft1 = reg.get(f.L1);
+        f.fft2 = reg.get(f.L2);
+        auto pick = [](int64_t n, int& tile, int& nt) {
+            // up to 16 transforms per workgroup, at most 8 elements per thread
+            for (int t : {256, 512, 1024}) {
+                if (16 * n <= 8 * t) { tile = 16; nt = t; return; }
+            }
+            nt = 1024;
+            tile = static_cast<int>(std::max<int64_t>(1, 8 * 1024 / n));
+        };
+        pick(f.L1, f.tile_a, f.nt_a);
+        pick(f.L2, f.tile_b, f.nt_b);
+        f.tile_a = static_cast<int>(std::min<int64_t>(f.tile_a, f.L2));
+        f.tile_b = static_cast<int>(std::min<int64_t>(f.tile_b, f.L1));
+        f.ld_a = static_cast<int>(f.L1 | 1);
+        f.ld_b = static_cast<int>(f.L2 | 1);
+        if (static_cast<int64_t>(f.tile_a) * f.ld_a * 8 > 160 * 1024 - 1024 ||
+            static_cast<int64_t>(f.tile_b) * f.ld_b * 8 > 160 * 1024 - 1024)
+            return fail(err, NSGCQT_EUNSUPPORTED, "four-step tile exceeds LDS");
+        int64_t s = 1;
+        while (s * s < L) ++s;
+        f.split = s;
+        p.tw4_hi.clear(); p.tw4_lo.clear();
+        for (int64_t i = 0; i * s < L; ++i) push_c(p.tw4_hi, root(i * s, L));
+        for (int64_t j = 0; j < s; ++j) push_c(p.tw4_lo, root(j, L));
+    }
+
+    // ---- band transforms: mixed radix, or Bluestein over a 7-smooth length
+    p.banddev.clear(); p.chirp.clear(); p.kern.clear();
+    std::vector<int> work(p.bands.size());
+    for (size_t l = 0; l < p.bands.size(); ++l) {
+        const auto& b = p.bands[l];
+        BandDev d{};
+        d.k_lo = static_cast<int32_t>(b.k_lo);
+        d.M = static_cast<int32_t>(b.M);
+        d.rot = static_cast<int32_t>(((b.k_lo - b.k_c) % b.M + b.M) % b.M);
+        d.off = static_cast<int32_t>(b.off);
+        d.inv_M = static_cast<float>(1.0 / static_cast<double>(b.M));
+        d.chirp = -1; d.kern = -1;
+        int id = reg.get(b.M);
+        if (id >= 0) {
+            d.fft = id;
+            work[l] = static_cast<int>(b.M);
+        } else {
+            const int64_t M = b.M;
+            const int64_t P = smooth7_at_least(2 * M - 1);
+            d.fft = reg.get(P);
+            if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no Bluestein length");
+            d.chirp = static_cast<int32_t>(p.chirp.size() / 2);
+            d.kern = static_cast<int32_t>(p.kern.size() / 2);
+            // chirp exp(-i pi m^2 / M), argument reduced exactly: m^2 mod 2M
+            std::vector<cd> ch(M);
+            for (int64_t m = 0; m < M; ++m) {
+                const int64_t t = (m * m) % (2 * M);
+                const double ang = kPi * static_cast<double>(t) / static_cast<double>(M);
+                ch[m] = cd(std::cos(ang), -std::sin(ang));
+                push_c(p.chirp, ch[m]);
+            }
+            // kernel b_P[t] = conj(chirp[|t|]) on the cyclic support |t| < M,
+            // transformed once and scaled by 1/P
+            std::vector<cd> bp(P, cd(0.0, 0.0));
+            for (int64_t t = 0; t < M; ++t) {
+                bp[t] = std::conj(ch[t]);
+                if (t) bp[P - t] = std::conj(ch[t]);
+            }
+            host_dft(bp);
+            for (int64_t t = 0; t < P; ++t) push_c(p.kern, bp[t] / static_cast<double>(P));
+            work[l] = static_cast<int>(P);
+        }
+        p.banddev.push_back(d);
+    }
+
+    // ---- buckets by transform length
+    struct Tier { int max_work, nt, ept; };
+    const Tier tiers[] = {{512, 64, 8}, {2048, 256, 8}, {8192, 1024, 8}, {16384, 1024, 16}};
+    p.buckets.clear();
+    for (const auto& t : tiers) {
+        Bucket bk{};
+        bk.nt = t.nt; bk.ept = t.ept; bk.max_work = 0; bk.coeffs = 0;
+        p.buckets.push_back(bk);
+    }
+    for (size_t l = 0; l < p.bands.size(); ++l) {
+        int ti = -1;
+        for (int i = 0; i < 4; ++i)
+            if (work[l] <= tiers[i].max_work) { ti = i; break; }
+        if (ti < 0)
+            return fail(err, NSGCQT_EUNSUPPORTED,
+                        "band of length " + std::to_string(p.bands[l].M) +
+                            " needs a transform of " + std::to_string(work[l]) +
+                            " points, above the 16384 one workgroup holds");
+        auto& bk = p.buckets[ti];
+        bk.bands.push_back(static_cast<int32_t>(l));
+        bk.max_work = std::max(bk.max_work, work[l]);
+        bk.coeffs += p.bands[l].M;
+    }
+    p.buckets.erase(std::remove_if(p.buckets.begin(), p.buckets.end(),
+                                   [](const Bucket& b) { return b.bands.empty(); }),
+                    p.buckets.end());
+    p.bucket_lists.clear();
+    for (auto& bk : p.buckets) {
+        bk.list_off = static_cast<int>(p.bucket_lists.size());
+        p.bucket_lists.insert(p.bucket_lists.end(), bk.bands.begin(), bk.bands.end());
+    }
+
+    // ---- slicing window (Sec. 4): zero, sin^2 rise, flat, cos^2 fall, zero
+    p.slicewin.clear();
+    if (sliced) {
+        const int64_t e = N / 8;
+        const double q = static_cast<double>(N) / 2.0;
+        for (int64_t t = 0; t < N; ++t) {
+            double w = 0.0;
+            if (t >= e && t < 3 * e) { const double s = std::sin(kPi * static_cast<double>(t - e) / q); w = s * s; }
+            else if (t >= 3 * e && t < 5 * e) w = 1.0;
+            else if (t >= 5 * e && t < 7 * e) { const double c = std::cos(kPi * static_cast<double>(t - 5 * e) / q); w = c * c; }
+            p.slicewin.push_back(static_cast<float>(w));
+        }
+    }
+
+    // ---- workspace
+    const int64_t b = batch;
+    p.ws_an = 2 * align256(8 * L * b);
+    p.ws_syn = align256(8 * p.C * b) + align256(8 * L * b);
+    if (sliced) p.ws_syn += align256(4 * N * b) + 2 * align256(4 * (N / 2));
+    return NSGCQT_OK;
+}
+
+}  // namespace nsg

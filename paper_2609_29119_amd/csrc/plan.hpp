@@ -1,0 +1,84 @@
+// Host-side plan: layout, windows, duals and every table the kernels read,
+// computed in fp64 and stored as fp32 (or int32) for upload.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "tables.hpp"
+
+namespace nsg {
+
+struct HostBand {
+    int kind;             // 0 DC, 1 positive, 2 Nyquist
+    int64_t k_lo, k_hi, k_c, M, off;
+    double f, xi, beta;
+    std::vector<double> g, h;   // on k_lo..k_hi
+};
+
+// Band kernels are launched per bucket; each bucket has one thread count and
+// one bound on the elements each thread holds per Stockham stage.
+struct Bucket {
+    int nt;               // threads per workgroup
+    int ept;              // elements per thread bound (template parameter)
+    int max_work;         // largest transform length in the bucket
+    int64_t coeffs;       // sum of M over its bands
+    std::vector<int32_t> bands;
+    int list_off;         // offset of its band list in the device list array
+};
+
+// Four-step split of the packed FFT: L = L1 * L2. Pass A transforms columns
+// (length L1, `tile_a` columns per workgroup), pass B rows (length L2,
+// `tile_b` rows per workgroup).
+struct FourStep {
+    int64_t L1, L2;
+    int fft1, fft2;       // FftDesc indices
+    int tile_a, tile_b;
+    int nt_a, nt_b;       // threads per workgroup of each pass
+    int ld_a, ld_b;       // LDS leading dimensions (padded)
+    int64_t split;        // omega_L^t = hi[t / split] * lo[t % split]
+};
+
+struct HostPlan {
+    // parameters
+    double fs = 0, fmin = 0, fmax = 0;
+    int bpo = 0;
+    int64_t N = 0, L = 0;
+    int batch = 0;
+    bool sliced = false;
+    int spc = 0;          // slices per chunk (sliced plans)
+
+    // layout
+    std::vector<HostBand> bands;
+    int64_t C = 0, maxM = 0;
+    int64_t max_fanout = 0, max_overlap = 0;
+    std::vector<double> a;
+
+    // fp32 tables
+    std::vector<float> wA, wS, wT, wSa;     // C each, bin order
+    std::vector<FftDesc> ffts;
+    std::vector<float> twpool;              // interleaved complex
+    std::vector<float> omega;               // exp(-2 pi i k / N), k = 0..L
+    std::vector<float> tw4_hi, tw4_lo;      // four-step twiddles
+    std::vector<int32_t> owner;             // per bin k = 0..L: first band | count << 24
+    std::vector<int32_t> bandbase;          // per band: off - k_lo
+    std::vector<BandDev> banddev;
+    std::vector<float> chirp, kern;         // Bluestein tables
+    std::vector<float> slicewin;            // sliced plans: window of length N
+    std::vector<Bucket> buckets;
+    std::vector<int32_t> bucket_lists;
+    FourStep fs4{};
+
+    int64_t ws_an = 0, ws_syn = 0;
+};
+
+// Returns 0 on success, or a negative nsgcqt status with `err` set.
+int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int bpo,
+                    int64_t N, int batch, bool sliced, std::string& err);
+
+// Radix factorisation used by the Stockham stages: true when n factors into
+// 2, 3, 4, 5, 7, 8 and primes up to kGenericMaxRadix.
+bool factor_radices(int64_t n, std::vector<int>& radices);
+
+}  // namespace nsg

@@ -1,0 +1,38 @@
+// Device-visible table records shared by the host plan builder and the HIP
+// kernels. Plain structs only: the host fills them in fp64 and stores fp32.
+#pragma once
+
+#include <cstdint>
+
+namespace nsg {
+
+// Largest prime handled by the direct odd-radix Stockham stage. Lengths with a
+// larger prime factor are transformed with Bluestein's chirp-z algorithm over a
+// 7-smooth length P >= 2M - 1.
+constexpr int kGenericMaxRadix = 61;
+constexpr int kMaxStages = 28;
+
+// One transform length n: Stockham stages of the given radices, applied in
+// order, and the offset of its twiddles omega_n^t = exp(-2 pi i t / n),
+// t = 0..n-1, in the twiddle pool.
+struct FftDesc {
+    int32_t n;
+    int32_t nstages;
+    int32_t tw;
+    int32_t max_generic;     // largest generic (odd prime >= 11) radix, 0 if none
+    int16_t radix[kMaxStages];
+};
+
+// One band of the layout as the band kernels see it.
+struct BandDev {
+    int32_t k_lo;      // first support bin
+    int32_t M;         // band length = support width
+    int32_t rot;       // slot of bin k_lo: (k_lo - k_c) mod M
+    int32_t off;       // first coefficient of the band in a row
+    int32_t fft;       // FftDesc index: length M, or P for Bluestein
+    int32_t chirp;     // -1, or offset of exp(-i pi m^2 / M), m < M, in the chirp pool
+    int32_t kern;      // offset of DFT_P(b)/P in the kernel pool (Bluestein only)
+    float inv_M;
+};
+
+}  // namespace nsg

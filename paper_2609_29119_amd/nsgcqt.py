@@ -1,0 +1,295 @@
+"""ctypes binding of libnsgcqt.so.
+
+Argument marshalling only: every step of the transform runs in the library's
+HIP kernels. torch is used for device memory and streams. The library must be
+built first (``python -m paper_2609_29119_amd.build``); importing the binding
+does not build or fall back to anything.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libnsgcqt.so")
+
+OK, EINVAL, ENOMEM, EDEVICE, EWORKSPACE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OP_ANALYSE, OP_SYNTHESISE, OP_ADJ_ANALYSIS, OP_ADJ_SYNTHESIS = 0, 1, 2, 3
+BAND_DC, BAND_POSITIVE, BAND_NYQUIST = 0, 1, 2
+WEIGHT_G, WEIGHT_H, WEIGHT_ADJ_ANALYSIS, WEIGHT_ADJ_SYNTHESIS = 0, 1, 2, 3
+
+_STATUS = {OK: "OK", EINVAL: "EINVAL", ENOMEM: "ENOMEM", EDEVICE: "EDEVICE",
+           EWORKSPACE: "EWORKSPACE", EUNSUPPORTED: "EUNSUPPORTED"}
+
+EXPORTS = [
+    "nsgcqt_plan_create", "nsgcqt_plan_create_host", "nsgcqt_sliced_plan_create",
+    "nsgcqt_sliced_plan_create_host", "nsgcqt_plan_destroy", "nsgcqt_plan_info",
+    "nsgcqt_band_info", "nsgcqt_plan_weights", "nsgcqt_analyse", "nsgcqt_synthesise",
+    "nsgcqt_adjoint", "nsgcqt_sliced_count", "nsgcqt_sliced_analyse",
+    "nsgcqt_sliced_synthesise", "nsgcqt_set_stage_events", "nsgcqt_stage_info",
+    "nsgcqt_last_error",
+]
+
+
+class NsgcqtError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class Info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "n_bands", "batch", "n_samples", "packed_len", "total_coeffs", "max_band_len",
+        "max_fanout", "max_overlap", "sliced", "ws_analyse", "ws_synthesise",
+        "ws_adjoint_analysis", "ws_adjoint_synthesis", "table_bytes", "device_tables")]
+
+
+class BandInfo(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int64), ("k_lo", ctypes.c_int64), ("k_hi", ctypes.c_int64),
+                ("k_centre", ctypes.c_int64), ("length", ctypes.c_int64), ("offset", ctypes.c_int64),
+                ("centre_hz", ctypes.c_double), ("xi", ctypes.c_double), ("beta", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_29119_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, D, I, V = ctypes.c_void_p, ctypes.c_int64, ctypes.c_double, ctypes.c_int, ctypes.c_void_p
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    sig = {
+        "nsgcqt_plan_create": [pp, D, D, D, I, I64, I],
+        "nsgcqt_plan_create_host": [pp, D, D, D, I, I64, I],
+        "nsgcqt_sliced_plan_create": [pp, D, D, D, I, I64, I],
+        "nsgcqt_sliced_plan_create_host": [pp, D, D, D, I, I64, I],
+        "nsgcqt_plan_destroy": [P],
+        "nsgcqt_plan_info": [P, ctypes.POINTER(Info)],
+        "nsgcqt_band_info": [P, I, ctypes.POINTER(BandInfo)],
+        "nsgcqt_plan_weights": [P, I, V, ctypes.c_size_t],
+        "nsgcqt_analyse": [P, V, V, V, ctypes.c_size_t, V],
+        "nsgcqt_synthesise": [P, V, V, V, ctypes.c_size_t, V],
+        "nsgcqt_adjoint": [P, I, V, V, V, ctypes.c_size_t, V],
+        "nsgcqt_sliced_count": [P, I64],
+        "nsgcqt_sliced_analyse": [P, V, I64, V, V, ctypes.c_size_t, V],
+        "nsgcqt_sliced_synthesise": [P, V, I64, V, V, ctypes.c_size_t, V],
+        "nsgcqt_set_stage_events": [P, ctypes.POINTER(ctypes.c_void_p), I],
+        "nsgcqt_stage_info": [P, I, I, ctypes.c_char_p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_double)],
+        "nsgcqt_last_error": [],
+    }
+    for name, args in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = ctypes.c_int
+    L.nsgcqt_sliced_count.restype = ctypes.c_int64
+    L.nsgcqt_last_error.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status):
+    if status != OK:
+        raise NsgcqtError(status, lib().nsgcqt_last_error().decode())
+    return status
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Plan:
+    """A transform plan: layout, device tables and workspace sizes.
+
+    Plan(fs, fmin, fmax, bins_per_octave, n_samples, batch) transforms
+    [batch][n_samples] float32 signals; Plan.sliced(...) builds a sliced
+    (streaming) plan. device=False builds the host tables only.
+    """
+
+    def __init__(self, fs, fmin, fmax, bins_per_octave, n_samples, batch=1, device=True, _sliced=False):
+        L = lib()
+        h = ctypes.c_void_p()
+        if _sliced:
+            fn = L.nsgcqt_sliced_plan_create if device else L.nsgcqt_sliced_plan_create_host
+        else:
+            fn = L.nsgcqt_plan_create if device else L.nsgcqt_plan_create_host
+        _check(fn(ctypes.byref(h), float(fs), float(fmin), float(fmax), int(bins_per_octave),
+                  int(n_samples), int(batch)))
+        self._h = h
+        self.info = Info()
+        _check(L.nsgcqt_plan_info(self._h, ctypes.byref(self.info)))
+        self.device = bool(self.info.device_tables)
+        self._ws = {}
+
+    @classmethod
+    def sliced(cls, fs, fmin, fmax, bins_per_octave, slice_len, slices_per_chunk=16, device=True):
+        return cls(fs, fmin, fmax, bins_per_octave, slice_len, slices_per_chunk, device, _sliced=True)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().nsgcqt_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------------- queries
+    @property
+    def n_bands(self):
+        return self.info.n_bands
+
+    @property
+    def n_coeffs(self):
+        return self.info.total_coeffs
+
+    @property
+    def n_samples(self):
+        return self.info.n_samples
+
+    @property
+    def batch(self):
+        return self.info.batch
+
+    def band(self, i) -> BandInfo:
+        b = BandInfo()
+        _check(lib().nsgcqt_band_info(self._h, int(i), ctypes.byref(b)))
+        return b
+
+    def bands(self):
+        return [self.band(i) for i in range(self.n_bands)]
+
+    def weights(self, which):
+        import numpy as np
+        out = np.empty(self.n_coeffs, dtype=np.float32)
+        _check(lib().nsgcqt_plan_weights(self._h, int(which), out.ctypes.data_as(ctypes.c_void_p), out.nbytes))
+        return out
+
+    def workspace_bytes(self, op):
+        i = self.info
+        return {OP_ANALYSE: i.ws_analyse, OP_SYNTHESISE: i.ws_synthesise,
+                OP_ADJ_ANALYSIS: i.ws_adjoint_analysis, OP_ADJ_SYNTHESIS: i.ws_adjoint_synthesis}[op]
+
+    def workspace(self, op, device=None):
+        """A cached uint8 device buffer big enough for `op`."""
+        import torch
+        need = max(1, self.workspace_bytes(op))
+        ws = self._ws.get(op)
+        if ws is None or ws.numel() < need:
+            ws = torch.empty(need, dtype=torch.uint8, device=device or "cuda")
+            self._ws[op] = ws
+        return ws
+
+    def stage_info(self, op):
+        """[(kernel name, algorithmic bytes per launch)] of one call of `op`."""
+        L = lib()
+        n = L.nsgcqt_stage_info(self._h, int(op), -1, None, 0, None)
+        if n < 0:
+            _check(n)
+        out = []
+        for i in range(n):
+            name = ctypes.create_string_buffer(64)
+            b = ctypes.c_double()
+            _check(min(0, L.nsgcqt_stage_info(self._h, int(op), i, name, 64, ctypes.byref(b))))
+            out.append((name.value.decode(), b.value))
+        return out
+
+    def set_stage_events(self, handles):
+        """Record HIP events between kernels (see nsgcqt_set_stage_events); None stops."""
+        if not handles:
+            _check(lib().nsgcqt_set_stage_events(self._h, None, 0))
+            return
+        arr = (ctypes.c_void_p * len(handles))(*handles)
+        _check(lib().nsgcqt_set_stage_events(self._h, arr, len(handles)))
+
+    # ---------------------------------------------------------------- compute
+    def _new(self, shape, dtype, like):
+        import torch
+        return torch.empty(shape, dtype=dtype, device=like.device)
+
+    def analyse(self, x, out=None, ws=None, stream=None):
+        """x [batch][N] float32 (cuda) -> coefficients [batch][C] complex64."""
+        import torch
+        self._expect(x, torch.float32, (self.batch, self.n_samples))
+        out = self._new((self.batch, self.n_coeffs), torch.complex64, x) if out is None else out
+        self._expect(out, torch.complex64, (self.batch, self.n_coeffs))
+        ws = self.workspace(OP_ANALYSE, x.device) if ws is None else ws
+        _check(lib().nsgcqt_analyse(self._h, _ptr(x), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+        return out
+
+    def synthesise(self, c, out=None, ws=None, stream=None):
+        """coefficients [batch][C] complex64 -> signals [batch][N] float32."""
+        import torch
+        self._expect(c, torch.complex64, (self.batch, self.n_coeffs))
+        out = self._new((self.batch, self.n_samples), torch.float32, c) if out is None else out
+        self._expect(out, torch.float32, (self.batch, self.n_samples))
+        ws = self.workspace(OP_SYNTHESISE, c.device) if ws is None else ws
+        _check(lib().nsgcqt_synthesise(self._h, _ptr(c), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+        return out
+
+    def adjoint(self, op, inp, out=None, ws=None, stream=None):
+        """OP_ADJ_ANALYSIS: [b][C] c64 -> [b][N] f32; OP_ADJ_SYNTHESIS: [b][N] f32 -> [b][C] c64."""
+        import torch
+        if op == OP_ADJ_ANALYSIS:
+            self._expect(inp, torch.complex64, (self.batch, self.n_coeffs))
+            shape, dt = (self.batch, self.n_samples), torch.float32
+        elif op == OP_ADJ_SYNTHESIS:
+            self._expect(inp, torch.float32, (self.batch, self.n_samples))
+            shape, dt = (self.batch, self.n_coeffs), torch.complex64
+        else:
+            raise ValueError("op must be OP_ADJ_ANALYSIS or OP_ADJ_SYNTHESIS")
+        out = self._new(shape, dt, inp) if out is None else out
+        self._expect(out, dt, shape)
+        ws = self.workspace(op, inp.device) if ws is None else ws
+        _check(lib().nsgcqt_adjoint(self._h, int(op), _ptr(inp), _ptr(out), _ptr(ws), ws.numel(),
+                                    _stream(stream)))
+        return out
+
+    def slice_count(self, n):
+        r = lib().nsgcqt_sliced_count(self._h, int(n))
+        if r < 0:
+            _check(int(r))
+        return int(r)
+
+    def sliced_analyse(self, x, out=None, ws=None, stream=None):
+        """One signal x [n] float32 -> slice coefficients [J][C] complex64."""
+        import torch
+        n = x.numel()
+        J = self.slice_count(n)
+        self._expect(x, torch.float32, (n,))
+        out = self._new((J, self.n_coeffs), torch.complex64, x) if out is None else out
+        self._expect(out, torch.complex64, (J, self.n_coeffs))
+        ws = self.workspace(OP_ANALYSE, x.device) if ws is None else ws
+        _check(lib().nsgcqt_sliced_analyse(self._h, _ptr(x), n, _ptr(out), _ptr(ws), ws.numel(),
+                                           _stream(stream)))
+        return out
+
+    def sliced_synthesise(self, c, n, out=None, ws=None, stream=None):
+        """Slice coefficients [J][C] complex64 -> signal [n] float32."""
+        import torch
+        J = self.slice_count(n)
+        self._expect(c, torch.complex64, (J, self.n_coeffs))
+        out = self._new((n,), torch.float32, c) if out is None else out
+        self._expect(out, torch.float32, (n,))
+        ws = self.workspace(OP_SYNTHESISE, c.device) if ws is None else ws
+        _check(lib().nsgcqt_sliced_synthesise(self._h, _ptr(c), int(n), _ptr(out), _ptr(ws), ws.numel(),
+                                              _stream(stream)))
+        return out
+
+    @staticmethod
+    def _expect(t, dtype, shape):
+        if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or not t.is_cuda:
+            raise ValueError(f"expected a contiguous cuda {dtype} tensor of shape {tuple(shape)}, "
+                             f"got {t.dtype} {tuple(t.shape)} on {t.device}")

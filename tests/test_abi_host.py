@@ -1,0 +1,211 @@
+"""CPU checks of the C-ABI library: exports, layout, tables, error paths.
+
+No compute call runs here (there is no GPU); plans are created host-only.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from oracle.layout import DC, NYQUIST, POSITIVE
+
+pn = pytest.importorskip("paper_2609_29119_amd")
+from paper_2609_29119_amd import nsgcqt as nb  # noqa: E402
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(nb.LIB_PATH):
+        pytest.fail("libnsgcqt.so is not built; run python -m paper_2609_29119_amd.build")
+    return nb.lib()
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "nsgcqt.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:int|int64_t|const char\*)\s+(nsgcqt_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = header_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(nb.EXPORTS) == names
+
+
+def _host_plan(w, n=None, batch=None):
+    return nb.Plan(w.fs, w.fmin, w.fmax, w.bins_per_octave, n or w.n_samples,
+                   batch or w.batch, device=False)
+
+
+LAYOUT_CASES = [(name, None) for name in ("tiny", "single", "train", "stress")] + [("long", 131072)]
+
+
+@pytest.mark.parametrize("name,n", LAYOUT_CASES)
+def test_integer_layout_identical_to_oracle(lib, name, n):
+    w = workloads.WORKLOADS[name]
+    N = n or w.n_samples
+    lay = oracle.build_layout(w.fs, w.fmin, w.fmax, w.bins_per_octave, N)
+    if n:
+        p = nb.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, N, 4, device=False)
+    else:
+        p = _host_plan(w)
+    assert p.n_bands == len(lay.bands)
+    assert p.n_coeffs == lay.n_coeffs
+    assert p.info.packed_len == N // 2
+    assert p.info.max_band_len == max(b.M for b in lay.bands)
+    for i, (ob, cb) in enumerate(zip(lay.bands, p.bands())):
+        assert (cb.kind, cb.k_lo, cb.k_hi, cb.k_centre, cb.length, cb.offset) == \
+               (ob.kind, ob.k_lo, ob.k_hi, ob.k_c, ob.M, ob.offset), i
+        assert cb.xi == ob.xi and cb.beta == ob.beta
+
+
+@pytest.mark.parametrize("name", ["tiny", "single", "stress"])
+def test_weight_tables_match_oracle(lib, name):
+    w = workloads.WORKLOADS[name]
+    lay = oracle.build_layout(*w.plan_args)
+    p = _host_plan(w)
+    N, half = lay.N, lay.half
+    g = np.concatenate([b.g for b in lay.bands])
+    h = np.concatenate([b.h for b in lay.bands])
+    k = np.concatenate([b.bins for b in lay.bands])
+    M = np.concatenate([np.full(b.M, b.M) for b in lay.bands])
+    d = np.where((k == 0) | (k == half), 1.0, 2.0)
+    ref = {nb.WEIGHT_G: g, nb.WEIGHT_H: h, nb.WEIGHT_ADJ_ANALYSIS: N / (d * M) * g,
+           nb.WEIGHT_ADJ_SYNTHESIS: M * d / N * h}
+    for which, r in ref.items():
+        got = p.weights(which).astype(np.float64)
+        np.testing.assert_allclose(got, r, rtol=1e-7, atol=1e-30)
+
+
+def _packed_eval(p, lay, x):
+    """Evaluate the packed factorisation (eqs. 5-10) in fp64 with the
+    library's band records and weight tables."""
+    N, L = lay.N, lay.N // 2
+    z = x[0::2] + 1j * x[1::2]                 # eq. 5
+    Z = np.fft.fft(z)
+    om = np.exp(-2j * np.pi * np.arange(L + 1) / N)
+    g = p.weights(nb.WEIGHT_G).astype(np.float64)
+    hw = p.weights(nb.WEIGHT_H).astype(np.float64)
+    C = p.n_coeffs
+    c = np.zeros(C, complex)
+    for b in p.bands():
+        k = np.arange(b.k_lo, b.k_hi + 1)
+        a = k % L
+        u = 0.5 * g[b.offset:b.offset + b.length] * ((1 - 1j * om[k]) * Z[a] + (1 + 1j * om[k]) * np.conj(Z[(-a) % L]))
+        v = np.zeros(b.length, complex)
+        v[(k - b.k_centre) % b.length] = u     # eq. 7 router, then eq. 8
+        c[b.offset:b.offset + b.length] = np.fft.ifft(v)
+    X = np.zeros(L + 1, complex)
+    for b in p.bands():
+        k = np.arange(b.k_lo, b.k_hi + 1)
+        U = np.fft.fft(c[b.offset:b.offset + b.length])
+        X[k] += hw[b.offset:b.offset + b.length] * U[(k - b.k_centre) % b.length]
+    X[0], X[L] = X[0].real, X[L].real
+    q = np.arange(L)
+    Zs = 0.5 * ((1 + 1j * np.conj(om[q])) * X[q] + (1 - 1j * np.conj(om[q])) * np.conj(X[L - q]))   # eq. 9
+    zr = np.fft.ifft(Zs)
+    xr = np.empty(N)
+    xr[0::2], xr[1::2] = zr.real, zr.imag     # P^{-1}
+    return c, xr
+
+
+@pytest.mark.parametrize("N,fs,fmin,fmax,B", [(500, 250.0, 4.0, 125.0, 4), (16384, 22050.0, 110.0, 11025.0, 12)])
+def test_library_tables_drive_packed_path(lib, N, fs, fmin, fmax, B):
+    lay = oracle.build_layout(fs, fmin, fmax, B, N)
+    p = nb.Plan(fs, fmin, fmax, B, N, 1, device=False)
+    x = workloads.white(7, 1, N)[0].astype(np.float64)
+    c, xr = _packed_eval(p, lay, x)
+    # the fp32 tables limit agreement to about 1e-7
+    assert oracle.rel_l2(c, oracle.analyse(lay, x)) < 3e-7
+    assert oracle.snr_db(x, xr) > 130.0
+
+
+def test_info_and_workspace(lib):
+    w = workloads.WORKLOADS["stress"]
+    p = _host_plan(w)
+    i = p.info
+    L, C, b = w.n_samples // 2, i.total_coeffs, w.batch
+    assert i.ws_analyse >= 16 * L * b
+    assert i.ws_synthesise >= 8 * C * b + 8 * L * b
+    assert i.device_tables == 0 and i.table_bytes == 0
+    assert i.max_overlap == 3 and i.max_fanout == 6
+    names = [n for n, _ in p.stage_info(nb.OP_ANALYSE)]
+    assert names[:2] == ["fft_fwd_a", "fft_fwd_b"] and all(n.startswith("band_analysis") for n in names[2:])
+    tot = sum(b_ for _, b_ in p.stage_info(nb.OP_ANALYSE))
+    assert tot == pytest.approx((16 + 16 + 8) * L * b + 8 * C * b)
+
+
+def _status(fn, *args):
+    h = ctypes.c_void_p()
+    return fn(ctypes.byref(h), *args), h
+
+
+@pytest.mark.parametrize("args", [
+    (22050.0, 110.0, 11025.0, 12, 16383, 1),     # odd N
+    (22050.0, 110.0, 11025.0, 12, 2, 1),         # N < 4
+    (0.0, 110.0, 11025.0, 12, 16384, 1),         # fs
+    (22050.0, 0.0, 11025.0, 12, 16384, 1),       # fmin <= 0
+    (22050.0, 11025.0, 11025.0, 12, 16384, 1),   # fmin >= fs/2
+    (22050.0, 110.0, 100.0, 12, 16384, 1),       # fmax < fmin
+    (22050.0, 110.0, 11025.0, 0, 16384, 1),      # bins per octave
+    (22050.0, 110.0, 11025.0, 12, 16384, 0),     # batch
+])
+def test_invalid_parameters(lib, args):
+    st, h = _status(lib.nsgcqt_plan_create_host, *args)
+    assert st == nb.EINVAL and not h.value
+    assert lib.nsgcqt_last_error()
+
+
+def test_empty_bands_dropped_identically(lib):
+    # 48 bins per octave at N = 256 gives low bands narrower than one bin;
+    # both implementations must drop the same empty bands and keep coverage
+    args = (8000.0, 40.0, 4000.0, 48, 256)
+    lay = oracle.build_layout(*args)
+    p = nb.Plan(*args, 1, device=False)
+    import math
+    K = sum(1 for j in range(10000) if 40.0 * 2.0 ** (j / 48) < 4000.0)
+    assert len(lay.bands) < K + 2            # some were dropped
+    assert p.n_bands == len(lay.bands)
+    assert [(b.k_lo, b.k_hi) for b in p.bands()] == [(b.k_lo, b.k_hi) for b in lay.bands]
+    assert np.all(lay.a > 0)
+
+
+def test_unsupported_packed_length(lib):
+    # L = 2 * 67 has a prime factor above the largest packed-FFT radix
+    st, _ = _status(lib.nsgcqt_plan_create_host, 268.0, 4.0, 134.0, 4, 268, 1)
+    assert st == nb.EUNSUPPORTED
+
+
+def test_sliced_plan_rules(lib):
+    st, _ = _status(lib.nsgcqt_sliced_plan_create_host, 48000.0, 20.0, 24000.0, 96, 131076, 4)
+    assert st == nb.EINVAL     # not a multiple of 8
+    p = nb.Plan.sliced(48000.0, 20.0, 24000.0, 96, 131072, 4, device=False)
+    assert p.slice_count(2880000) == oracle.slice_count(2880000, 131072) == 45
+    assert p.slice_count(1) == 2
+
+
+def test_compute_calls_reject_bad_arguments(lib):
+    w = workloads.WORKLOADS["tiny"]
+    p = _host_plan(w)
+    h = p._h
+    buf = ctypes.c_void_p(16)      # never dereferenced: every call fails validation first
+    need = p.info.ws_analyse
+    assert lib.nsgcqt_analyse(None, buf, buf, buf, need, None) == nb.EINVAL
+    assert lib.nsgcqt_analyse(h, None, buf, buf, need, None) == nb.EINVAL
+    assert lib.nsgcqt_analyse(h, buf, buf, buf, need - 1, None) == nb.EWORKSPACE
+    assert lib.nsgcqt_synthesise(h, buf, buf, buf, p.info.ws_synthesise - 1, None) == nb.EWORKSPACE
+    assert lib.nsgcqt_adjoint(h, 7, buf, buf, buf, need, None) == nb.EINVAL
+    assert lib.nsgcqt_sliced_analyse(h, buf, 100, buf, buf, need, None) == nb.EINVAL   # not sliced
+    # a host-only plan with valid arguments has no device tables
+    assert lib.nsgcqt_analyse(h, buf, buf, buf, need, None) == nb.EINVAL
+    assert b"host-only" in lib.nsgcqt_last_error()
+    assert lib.nsgcqt_band_info(h, p.n_bands, ctypes.byref(nb.BandInfo())) == nb.EINVAL
+    assert lib.nsgcqt_plan_weights(h, 9, buf, 1 << 20) == nb.EINVAL
+    assert lib.nsgcqt_plan_destroy(None) == nb.OK

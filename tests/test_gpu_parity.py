@@ -1,0 +1,194 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Bars (fp32 path vs fp64 oracle on the same fp32 inputs):
+  * coefficients and adjoint outputs: relative L2 <= 1e-5 per signal;
+  * reconstruction S(T x): SNR >= 120 dB per signal;
+  * run-to-run results bitwise identical (no atomics anywhere).
+Full-size workloads run in the launch configuration the benchmark times; the
+oracle then checks a sample of the batch (every band of those signals).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+torch = pytest.importorskip("torch")
+from paper_2609_29119_amd import nsgcqt as nb  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+REL_TOL = 1e-5
+SNR_MIN = 120.0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nb.lib()
+
+
+def to_gpu(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_np(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+# (name, fs, fmin, fmax, bins/oct, N, batch): small layouts spanning several
+# tiles, ragged tails, odd packed lengths, generic radices and Bluestein bands
+SMALL = [
+    ("N500_L250", 250.0, 4.0, 125.0, 4, 500, 2),
+    ("N250_oddL", 250.0, 4.0, 125.0, 3, 250, 1),
+    ("N4620_radix11", 4620.0, 30.0, 2310.0, 12, 4620, 3),
+    ("N6000_b5", 8000.0, 50.0, 4000.0, 24, 6000, 5),
+    ("tiny", 22050.0, 110.0, 11025.0, 12, 16384, 1),
+    ("tiny_b3", 22050.0, 110.0, 11025.0, 12, 16384, 3),
+    ("single", 44100.0, 32.7, 22050.0, 48, 44100, 1),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_analysis_synthesis_adjoints_small(case):
+    name, fs, fmin, fmax, B, N, b = case
+    lay = oracle.build_layout(fs, fmin, fmax, B, N)
+    p = nb.Plan(fs, fmin, fmax, B, N, b)
+    w = workloads.WORKLOADS["single"] if name == "single" else None
+    x = workloads.signals(w) if w else workloads.white(11 + N, b, N)
+    c = p.analyse(to_gpu(x))
+    cg = to_np(c)
+    cref = oracle.analyse(lay, x)
+    assert oracle.rel_l2(cg, cref).max() <= REL_TOL
+    xr = to_np(p.synthesise(c))
+    assert oracle.snr_db(x, xr).min() >= SNR_MIN
+    # synthesis of arbitrary coefficients
+    y = workloads.coeff_cotangent(21 + N, b, p.n_coeffs)
+    np.testing.assert_array_less(oracle.rel_l2(to_np(p.synthesise(to_gpu(y))), oracle.synthesise(lay, y)), REL_TOL)
+    # adjoints
+    ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
+    assert oracle.rel_l2(ta, oracle.adjoint_analysis(lay, y)).max() <= REL_TOL
+    xs = workloads.signal_cotangent(31 + N, b, N)
+    sa = to_np(p.adjoint(nb.OP_ADJ_SYNTHESIS, to_gpu(xs)))
+    assert oracle.rel_l2(sa, oracle.adjoint_synthesis(lay, xs)).max() <= REL_TOL
+
+
+def test_cosine_closed_form_on_gpu():
+    # a cosine at an integer bin lands in the bands holding that bin with
+    # |c| = N g / (2 M) (Sec. 2, eqs. 2-3), every other band ~ 0
+    fs, fmin, fmax, B, N = 22050.0, 110.0, 11025.0, 12, 16384
+    lay = oracle.build_layout(fs, fmin, fmax, B, N)
+    p = nb.Plan(fs, fmin, fmax, B, N, 1)
+    k0 = 1234
+    x = np.cos(2 * np.pi * k0 * np.arange(N) / N + 0.3).astype(np.float32)[None]
+    cg = to_np(p.analyse(to_gpu(x)))[0]
+    for b in lay.bands:
+        cb = cg[b.offset:b.offset + b.M]
+        if b.k_lo <= k0 <= b.k_hi:
+            ref = N * b.g[k0 - b.k_lo] / (2 * b.M)
+            np.testing.assert_allclose(np.abs(cb), ref, rtol=1e-4)
+        else:
+            assert np.abs(cb).max() < 1e-4
+
+
+def test_determinism_and_batch_position():
+    fs, fmin, fmax, B, N = 22050.0, 110.0, 11025.0, 12, 16384
+    p3 = nb.Plan(fs, fmin, fmax, B, N, 3)
+    p1 = nb.Plan(fs, fmin, fmax, B, N, 1)
+    x = workloads.white(5, 3, N)
+    xg = to_gpu(x)
+    a = to_np(p3.analyse(xg))
+    b = to_np(p3.analyse(xg))
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    one = to_np(p1.analyse(to_gpu(x[2:3])))
+    assert np.array_equal(one[0].view(np.uint32), a[2].view(np.uint32))
+    s1 = to_np(p3.synthesise(p3.analyse(xg)))
+    s2 = to_np(p3.synthesise(p3.analyse(xg)))
+    assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+
+
+def test_adjoint_identity_fp32():
+    w = workloads.WORKLOADS["tiny"]
+    p = nb.Plan(*w.plan_args, batch=2)
+    x = workloads.white(3, 2, w.n_samples)
+    y = workloads.coeff_cotangent(4, 2, p.n_coeffs)
+    tx = to_np(p.analyse(to_gpu(x))).astype(np.complex128)
+    ty = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y))).astype(np.float64)
+    lhs = np.sum(np.real(np.conj(tx) * y))
+    rhs = np.sum(x.astype(np.float64) * ty)
+    assert abs(lhs - rhs) <= 1e-5 * (np.linalg.norm(tx) * np.linalg.norm(y))
+    sy = to_np(p.synthesise(to_gpu(y))).astype(np.float64)
+    sx = to_np(p.adjoint(nb.OP_ADJ_SYNTHESIS, to_gpu(x))).astype(np.complex128)
+    lhs = np.sum(sy * x)
+    rhs = np.sum(np.real(np.conj(y) * sx))
+    assert abs(lhs - rhs) <= 1e-5 * (np.linalg.norm(sy) * np.linalg.norm(x))
+
+
+@pytest.mark.parametrize("name", ["stress", "train"])
+def test_full_size_workloads_sampled(name):
+    w = workloads.WORKLOADS[name]
+    lay = oracle.build_layout(*w.plan_args)
+    p = nb.Plan(*w.plan_args, batch=w.batch)
+    x = workloads.signals(w)
+    xg = to_gpu(x)
+    c = p.analyse(xg)
+    xr = to_np(p.synthesise(c))
+    cg = to_np(c)
+    assert oracle.snr_db(x, xr).min() >= SNR_MIN          # every signal of the batch
+    pick = sorted({0, 1, w.batch // 2, w.batch - 1})
+    assert oracle.rel_l2(cg[pick], oracle.analyse(lay, x[pick])).max() <= REL_TOL
+    y = workloads.coeff_cotangent(w.cot_seed, w.batch, p.n_coeffs)
+    ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
+    assert oracle.rel_l2(ta[pick], oracle.adjoint_analysis(lay, y[pick])).max() <= REL_TOL
+
+
+def test_sliced_mode_against_oracle():
+    w = workloads.WORKLOADS["long"]
+    Ns = w.slice_len
+    lay = oracle.build_layout(w.fs, w.fmin, w.fmax, w.bins_per_octave, Ns)
+    p = nb.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, Ns, 4)
+    n = 300001                       # odd length, several chunks of 4 slices
+    x = workloads.white(w.seed, 1, n)[0]
+    c = p.sliced_analyse(to_gpu(x))
+    cg = to_np(c)
+    J = oracle.slice_count(n, Ns)
+    assert cg.shape == (J, lay.n_coeffs)
+    cref = oracle.sliced_analyse(lay, x)
+    assert oracle.rel_l2(cg, cref).max() <= REL_TOL
+    xr = to_np(p.sliced_synthesise(c, n))
+    assert oracle.snr_db(x, xr) >= SNR_MIN
+    np.testing.assert_array_less(oracle.rel_l2(xr, oracle.sliced_synthesise(lay, cref, n)), 1e-5)
+
+
+def test_sliced_long_full_length():
+    # the 60 s workload: 45 slices in chunks of 16; oracle on sampled slices,
+    # reconstruction over the whole signal
+    w = workloads.WORKLOADS["long"]
+    Ns = w.slice_len
+    lay = oracle.build_layout(w.fs, w.fmin, w.fmax, w.bins_per_octave, Ns)
+    p = nb.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, Ns, 16)
+    x = workloads.signals(w)[0]
+    n = x.size
+    c = p.sliced_analyse(to_gpu(x))
+    xr = to_np(p.sliced_synthesise(c, n))
+    assert oracle.snr_db(x, xr) >= SNR_MIN
+    cg = to_np(c)
+    H = Ns // 2
+    xp = np.zeros((oracle.slice_count(n, Ns) + 1) * H)
+    xp[H:H + n] = x
+    win = oracle.slice_window(Ns)
+    for s in (0, 17, 44):
+        ref = oracle.analyse(lay, win * xp[s * H:s * H + Ns])
+        assert oracle.rel_l2(cg[s], ref) <= REL_TOL
+
+
+def test_workspace_too_small_raises():
+    w = workloads.WORKLOADS["tiny"]
+    p = nb.Plan(*w.plan_args, batch=1)
+    x = to_gpu(workloads.white(1, 1, w.n_samples))
+    ws = torch.empty(p.info.ws_analyse - 256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(nb.NsgcqtError) as e:
+        p.analyse(x, ws=ws)
+    assert e.value.status == nb.EWORKSPACE
