@@ -74,18 +74,21 @@ def traffic_from_profiles(workload, kernel):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, x):
-    """The fp64 oracle's round trip on a bounded sample of the batch."""
+def cpu_baseline(w, x, target_s=12.0):
+    """The fp64 oracle's round trip (analysis + synthesis) timed on a bounded
+    sample of the batch: signal counts double until one run takes about
+    target_s seconds (capped at the whole batch), and that run is reported."""
     import oracle
     from threadpoolctl import threadpool_info
     lay = oracle.build_layout(*w.plan_args)
-    t0 = time.perf_counter()
-    oracle.synthesise(lay, oracle.analyse(lay, x[:1]))
-    t1 = time.perf_counter() - t0
-    k = int(max(1, min(x.shape[0], round(15.0 / max(t1, 1e-3)))))
-    t0 = time.perf_counter()
-    oracle.synthesise(lay, oracle.analyse(lay, x[:k]))
-    dt = time.perf_counter() - t0
+    k = 1
+    while True:
+        t0 = time.perf_counter()
+        oracle.synthesise(lay, oracle.analyse(lay, x[:k]))
+        dt = time.perf_counter() - t0
+        if dt >= target_s or k >= x.shape[0]:
+            break
+        k = min(x.shape[0], max(2 * k, int(k * target_s / max(dt, 1e-3))))
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": k * w.n_samples / dt, "unit": "samples/s", "cores": int(threads),
             "kind": "oracle",

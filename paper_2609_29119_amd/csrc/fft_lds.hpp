@@ -137,73 +137,156 @@ template <int R> struct DftOdd {
 template <> struct Dft<5> { __device__ __forceinline__ static void run(float2* v) { DftOdd<5>::run(v); } };
 template <> struct Dft<7> { __device__ __forceinline__ static void run(float2* v) { DftOdd<7>::run(v); } };
 
+// ------------------------------------------------------------------ helpers
+
+// The thread index made opaque to the optimiser. Each stage derives its
+// indices from a fresh copy, so values of different stage kinds are not
+// hoisted out of the stage loop and kept live together (which otherwise
+// doubles the register footprint).
+__device__ __forceinline__ int stage_tid() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
+
+// LDS slot of element i: one pad slot after every 8 complex values, which
+// breaks the power-of-two strides of Stockham writes across the banks.
+__device__ __forceinline__ int lp(int i) { return i + (i >> 3); }
+
+// Exact quotient and remainder of 0 <= x < 2^22 by 0 < d < 2^22 through a
+// float reciprocal: the product is within one unit of x/d, fixed by one step.
+struct Div {
+    float r;
+    int d;
+};
+__device__ __forceinline__ Div mkdiv(int d) { return Div{1.0f / static_cast<float>(d), d}; }
+__device__ __forceinline__ int qdiv(int x, Div v, int& rem) {
+    int q = static_cast<int>(static_cast<float>(x) * v.r);
+    int r = x - q * v.d;
+    if (r < 0) { --q; r += v.d; }
+    else if (r >= v.d) { ++q; r -= v.d; }
+    rem = r;
+    return q;
+}
+
+// Odd prime radix with the symmetric pairing of DftOdd; cos/sin of 2 pi u/R
+// are read from the twiddle table (tw[u m] = omega_R^u), a uniform address.
+template <int R> struct DftOddT {
+    __device__ __forceinline__ static void run(float2* v, const float2* __restrict__ tw, int m) {
+        constexpr int h = (R - 1) / 2;
+        float cs[h + 1], sn[h + 1];
+#pragma unroll
+        for (int u = 1; u <= h; ++u) {
+            const float2 w = tw[u * m];
+            cs[u] = w.x;
+            sn[u] = -w.y;
+        }
+        float2 s[h + 1], d[h + 1];
+#pragma unroll
+        for (int r = 1; r <= h; ++r) {
+            s[r] = cadd(v[r], v[R - r]);
+            d[r] = csub(v[r], v[R - r]);
+        }
+        const float2 v0 = v[0];
+        float2 x0 = v0;
+#pragma unroll
+        for (int r = 1; r <= h; ++r) x0 = cadd(x0, s[r]);
+#pragma unroll
+        for (int q = 1; q <= h; ++q) {
+            float2 A = v0, B = make_float2(0.f, 0.f);
+#pragma unroll
+            for (int r = 1; r <= h; ++r) {
+                const int t = (r * q) % R;
+                const int u = t <= h ? t : R - t;
+                const float c = cs[u];
+                const float sg = t <= h ? sn[u] : -sn[u];
+                A.x += s[r].x * c; A.y += s[r].y * c;
+                B.x += d[r].x * sg; B.y += d[r].y * sg;
+            }
+            v[q] = make_float2(A.x + B.y, A.y - B.x);
+            v[R - q] = make_float2(A.x - B.y, A.y + B.x);
+        }
+        v[0] = x0;
+    }
+};
+
+template <int R> struct Radix {
+    __device__ __forceinline__ static void run(float2* v, const float2* __restrict__, int) { Dft<R>::run(v); }
+};
+template <> struct Radix<11> { __device__ __forceinline__ static void run(float2* v, const float2* tw, int m) { DftOddT<11>::run(v, tw, m); } };
+template <> struct Radix<13> { __device__ __forceinline__ static void run(float2* v, const float2* tw, int m) { DftOddT<13>::run(v, tw, m); } };
+
 // -------------------------------------------------------------------- stages
 
-// Stockham stage with compile-time radix R. Butterfly jj of transform t reads
-// in[jj + r m] (m = n/R), multiplies input r by omega_{Ns R}^{r k} (k = jj mod Ns),
-// and writes out[(jj - k) R + k + r Ns].
+// Stockham stage with compile-time radix R over nb sequences of length n at
+// LDS slots lp(t*ld + i). Butterfly jj of sequence t reads in[jj + r m]
+// (m = n/R), multiplies input r by omega_{Ns R}^{r k} (k = jj mod Ns), applies
+// the length-R DFT, and after a barrier writes out[(jj - k) R + k + r Ns].
 template <int R, int NT, int EPT>
 __device__ __forceinline__ void stage_fixed(float2* buf, int nb, int ld, int n, int Ns,
                                             const float2* __restrict__ tw) {
     constexpr int BPT = (EPT + R - 1) / R;
+    const int tid = stage_tid();
     const int m = n / R;
     const int total = nb * m;
     const int stride = n / (Ns * R);
+    const Div dm = mkdiv(m), dns = mkdiv(Ns);
     float2 v[BPT][R];
+    int ob[BPT];
 #pragma unroll
     for (int b = 0; b < BPT; ++b) {
-        const int j = threadIdx.x + b * NT;
+        const int j = tid + b * NT;
+        ob[b] = -1;
         if (j < total) {
-            const int t = j / m;
-            const int jj = j - t * m;
-            const float2* src = buf + t * ld + jj;
+            int jj, k;
+            const int t = qdiv(j, dm, jj);
+            qdiv(jj, dns, k);
+            const int src = t * ld + jj;
 #pragma unroll
-            for (int r = 0; r < R; ++r) v[b][r] = src[r * m];
+            for (int r = 0; r < R; ++r) v[b][r] = buf[lp(src + r * m)];
+            if (Ns > 1) {
+#pragma unroll
+                for (int r = 1; r < R; ++r) v[b][r] = cmul(v[b][r], tw[r * k * stride]);
+            }
+            Radix<R>::run(v[b], tw, m);
+            ob[b] = t * ld + (jj - k) * R + k;
         }
     }
     __syncthreads();
 #pragma unroll
     for (int b = 0; b < BPT; ++b) {
-        const int j = threadIdx.x + b * NT;
-        if (j < total) {
-            const int t = j / m;
-            const int jj = j - t * m;
-            const int k = jj % Ns;
-            if (Ns > 1) {
+        if (ob[b] >= 0) {
 #pragma unroll
-                for (int r = 1; r < R; ++r) v[b][r] = cmul(v[b][r], tw[r * k * stride]);
-            }
-            Dft<R>::run(v[b]);
-            float2* dst = buf + t * ld + (jj - k) * R + k;
-#pragma unroll
-            for (int r = 0; r < R; ++r) dst[r * Ns] = v[b][r];
+            for (int r = 0; r < R; ++r) buf[lp(ob[b] + r * Ns)] = v[b][r];
         }
     }
     __syncthreads();
 }
 
-// Stockham stage for an odd prime radix R (11 <= R <= kGenericMaxRadix) known
+// Stockham stage for an odd prime radix R (17 <= R <= kGenericMaxRadix) known
 // only at run time. Inputs are first multiplied by their stage twiddles in
 // place; then each work item (butterfly, q) produces the output pair q, R-q by
 // the symmetric sums of DftOdd, reading the twiddled inputs from LDS.
 template <int NT, int EPT>
 __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n, int Ns, int R,
-                                           const float2* __restrict__ tw, float2* wr) {
+                                              const float2* __restrict__ tw, float2* wr) {
     constexpr int IPT = (EPT * 6 + 9) / 10;   // items <= nb n (R+1)/(2R) <= 0.55 NT EPT
+    const int tid = stage_tid();
     const int m = n / R;
     const int h = (R - 1) >> 1;
     const int stride = n / (Ns * R);
-    for (int t = threadIdx.x; t < R; t += NT) wr[t] = tw[t * m];   // omega_R^t
+    const Div dn = mkdiv(n), dm = mkdiv(m), dns = mkdiv(Ns), dhp = mkdiv(h + 1);
+    for (int t = tid; t < R; t += NT) wr[t] = tw[t * m];   // omega_R^t
     if (Ns > 1) {
         const int tot = nb * n;
-        for (int e = threadIdx.x; e < tot; e += NT) {
-            const int t = e / n;
-            const int i = e - t * n;
-            const int r = i / m;
+        for (int e = tid; e < tot; e += NT) {
+            int i, jj, k;
+            const int t = qdiv(e, dn, i);
+            const int r = qdiv(i, dm, jj);
             if (r) {
-                const int k = (i - r * m) % Ns;
-                float2* p = buf + t * ld + i;
-                *p = cmul(*p, tw[r * k * stride]);
+                qdiv(jj, dns, k);
+                const int a = lp(t * ld + i);
+                buf[a] = cmul(buf[a], tw[r * k * stride]);
             }
         }
     }
@@ -211,21 +294,23 @@ __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n
     const int hp = h + 1;
     const int items = nb * m * hp;
     float2 o0[IPT], o1[IPT];
+    int ob[IPT], oq[IPT];
 #pragma unroll
     for (int b = 0; b < IPT; ++b) {
-        const int it = threadIdx.x + b * NT;
+        const int it = tid + b * NT;
+        ob[b] = -1;
         if (it < items) {
-            const int q = it % hp;
-            const int j = it / hp;
-            const int t = j / m;
-            const int jj = j - t * m;
-            const float2* src = buf + t * ld + jj;
-            float2 A = src[0], B = make_float2(0.f, 0.f);
+            int q, jj, k;
+            const int j = qdiv(it, dhp, q);
+            const int t = qdiv(j, dm, jj);
+            qdiv(jj, dns, k);
+            const int src = t * ld + jj;
+            float2 A = buf[lp(src)], B = make_float2(0.f, 0.f);
             int idx = 0;
             for (int r = 1; r <= h; ++r) {
                 idx += q;
                 if (idx >= R) idx -= R;
-                const float2 a = src[r * m], c = src[(R - r) * m];
+                const float2 a = buf[lp(src + r * m)], c = buf[lp(src + (R - r) * m)];
                 const float2 w = wr[idx];        // (cos, -sin) of 2 pi idx / R
                 A.x += (a.x + c.x) * w.x;
                 A.y += (a.y + c.y) * w.x;
@@ -234,32 +319,27 @@ __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n
             }
             o0[b] = make_float2(A.x + B.y, A.y - B.x);
             o1[b] = make_float2(A.x - B.y, A.y + B.x);
+            ob[b] = t * ld + (jj - k) * R + k;
+            oq[b] = q;
         }
     }
     __syncthreads();
 #pragma unroll
     for (int b = 0; b < IPT; ++b) {
-        const int it = threadIdx.x + b * NT;
-        if (it < items) {
-            const int q = it % hp;
-            const int j = it / hp;
-            const int t = j / m;
-            const int jj = j - t * m;
-            const int k = jj % Ns;
-            float2* dst = buf + t * ld + (jj - k) * R + k;
-            dst[q * Ns] = o0[b];
-            if (q) dst[(R - q) * Ns] = o1[b];
+        if (ob[b] >= 0) {
+            buf[lp(ob[b] + oq[b] * Ns)] = o0[b];
+            if (oq[b]) buf[lp(ob[b] + (R - oq[b]) * Ns)] = o1[b];
         }
     }
     __syncthreads();
 }
 
-// Forward DFTs of nb sequences of length d->n at buf + t*ld. `wr` is LDS
-// scratch for kGenericMaxRadix complex values. Ends with a barrier (when
-// there is at least one stage).
+// Forward DFTs of nb sequences of length d->n at LDS slots lp(t*ld + i). `wr`
+// is LDS scratch for kGenericMaxRadix complex values. Ends with a barrier
+// (when there is at least one stage).
 template <int NT, int EPT>
 __device__ __forceinline__ void lds_fft(float2* buf, int nb, int ld, const FftDesc* __restrict__ d,
-                        const float2* __restrict__ twpool, float2* wr) {
+                                        const float2* __restrict__ twpool, float2* wr) {
     const int n = d->n;
     const int ns = d->nstages;
     const float2* tw = twpool + d->tw;
@@ -273,6 +353,8 @@ __device__ __forceinline__ void lds_fft(float2* buf, int nb, int ld, const FftDe
             case 3: stage_fixed<3, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
             case 5: stage_fixed<5, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
             case 7: stage_fixed<7, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
+            case 11: stage_fixed<11, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
+            case 13: stage_fixed<13, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
             default: stage_generic<NT, EPT>(buf, nb, ld, n, Ns, R, tw, wr); break;
         }
         Ns *= R;

@@ -31,7 +31,7 @@ struct Tables {
     const float2* tw4_hi;
     const float2* tw4_lo;
     const float* slicewin;
-    const int32_t* lists;    // band lists of the buckets
+    const WorkItem* items;   // work items of the band kernels, all buckets
 };
 
 struct Pass {
@@ -70,7 +70,7 @@ __device__ __forceinline__ float2 tw4(const Tables& T, int t, int split) {
 // writes Y[k1 L2 + n2].
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
-                                              Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
+                                                      Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
     float2* buf = lds + kWrSlots;
@@ -80,32 +80,36 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
     const int n2a = tile * p.tile;
     const int cols = min(p.tile, p.L2 - n2a);
     const int tot = cols * p.L1;
+    const Div dc = mkdiv(cols);
     if (!sl.enabled) {
         const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
         for (int e = threadIdx.x; e < tot; e += NT) {
-            const int c = e % cols, n1 = e / cols;
-            buf[c * p.ld + n1] = z[(long long)n1 * p.L2 + n2a + c];
+            int c;
+            const int n1 = qdiv(e, dc, c);
+            buf[lp(c * p.ld + n1)] = z[(long long)n1 * p.L2 + n2a + c];
         }
     } else {
         // padded coordinate of sample 2j of slice s is s H + 2j; the signal
         // starts at padded H
         const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
         for (int e = threadIdx.x; e < tot; e += NT) {
-            const int c = e % cols, n1 = e / cols;
+            int c;
+            const int n1 = qdiv(e, dc, c);
             const long long j = (long long)n1 * p.L2 + n2a + c;
             const long long t = base + 2 * j;
             const float v0 = (t >= 0 && t < sl.n) ? x[t] : 0.f;
             const float v1 = (t + 1 >= 0 && t + 1 < sl.n) ? x[t + 1] : 0.f;
-            buf[c * p.ld + n1] = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
+            buf[lp(c * p.ld + n1)] = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
         }
     }
     __syncthreads();
     lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr);
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        const int c = e % cols, k1 = e / cols;
+        int c;
+        const int k1 = qdiv(e, dc, c);
         const int n2 = n2a + c;
-        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[c * p.ld + k1], tw4(T, n2 * k1, p.split));
+        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[lp(c * p.ld + k1)], tw4(T, n2 * k1, p.split));
     }
 }
 
@@ -126,7 +130,7 @@ __device__ __forceinline__ float2 gather_bin(const Tables& T, const float2* __re
 // The inverse DFT is taken as conj(F_L conj(Z)) / L.
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
-                                              Pass p, Tables T, int batch, long long C) {
+                                                      Pass p, Tables T, int batch, long long C) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
     float2* buf = lds + kWrSlots;
@@ -136,9 +140,11 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     const int n2a = tile * p.tile;
     const int cols = min(p.tile, p.L2 - n2a);
     const int tot = cols * p.L1;
+    const Div dc = mkdiv(cols);
     const float2* Ws = W + (long long)sig * C;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        const int c = e % cols, n1 = e / cols;
+        int c;
+        const int n1 = qdiv(e, dc, c);
         const int q = n1 * p.L2 + n2a + c;
         float2 xq = gather_bin(T, Ws, q);
         float2 xm = gather_bin(T, Ws, p.L - q);
@@ -147,15 +153,16 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
         const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w)
         const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
         const float2 zq = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
-        buf[c * p.ld + n1] = make_float2(0.5f * zq.x, -0.5f * zq.y);   // conj(Z_q)
+        buf[lp(c * p.ld + n1)] = make_float2(0.5f * zq.x, -0.5f * zq.y);   // conj(Z_q)
     }
     __syncthreads();
     lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr);
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        const int c = e % cols, k1 = e / cols;
+        int c;
+        const int k1 = qdiv(e, dc, c);
         const int n2 = n2a + c;
-        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[c * p.ld + k1], tw4(T, n2 * k1, p.split));
+        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[lp(c * p.ld + k1)], tw4(T, n2 * k1, p.split));
     }
 }
 
@@ -165,8 +172,8 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
 // INVERSE = true : z_k = conj(result) / L, unpacked to x_{2k}, x_{2k+1} (P^{-1}).
 template <int NT, int EPT, bool INVERSE>
 __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict__ Y, float2* __restrict__ out,
-                                               Pass p, Tables T, int batch, long long out_stride,
-                                               float inv_L) {
+                                                       Pass p, Tables T, int batch, long long out_stride,
+                                                       float inv_L) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
     float2* buf = lds + kWrSlots;
@@ -176,25 +183,28 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
     const int k1a = tile * p.tile;
     const int rows = min(p.tile, p.L1 - k1a);
     const int tot = rows * p.L2;
+    const Div dl2 = mkdiv(p.L2), drows = mkdiv(rows);
     const float2* Ys = Y + (long long)sig * p.L + (long long)k1a * p.L2;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        const int r = e / p.L2, n2 = e - r * p.L2;
-        buf[r * p.ld + n2] = Ys[e];
+        int n2;
+        const int r = qdiv(e, dl2, n2);
+        buf[lp(r * p.ld + n2)] = Ys[e];
     }
     __syncthreads();
     lds_fft<NT, EPT>(buf, rows, p.ld, T.ffts + p.fft, T.tw, wr);
     float2* os = out + (long long)sig * out_stride;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        const int r = e % rows, k2 = e / rows;
+        int r;
+        const int k2 = qdiv(e, drows, r);
         const long long k = (long long)k1a + r + (long long)p.L1 * k2;
-        const float2 v = buf[r * p.ld + k2];
+        const float2 v = buf[lp(r * p.ld + k2)];
         os[k] = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
     }
 }
 
 // ------------------------------------------------------------ band analysis
-// One workgroup per (band, signal). For entry i of the band (bin k = k_lo + i)
-// the router (eq. 7) forms
+// One workgroup per work item (band, signals s0 .. s0 + count - 1). For entry i
+// of the band (bin k = k_lo + i) the router (eq. 7) forms
 //   u = (1/2) w [(1 - i w_k) Z_{k mod L} + (1 + i w_k) conj(Z_{-k mod L})]
 // with w the band's weight at k (g for T, the S^dagger weight for S^dagger),
 // places conj(u) at slot (k - k_c) mod M in LDS, and the band's inverse DFT
@@ -204,21 +214,24 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
 // cyclic chirp exp(+i pi t^2/M), |t| < M.
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __restrict__ Z, float2* __restrict__ coef,
-                                                      const float* __restrict__ wt, Tables T, int list_off,
-                                                      int nbl, int batch, int L, long long C) {
+                                                              const float* __restrict__ wt, Tables T, int item0,
+                                                              int nitems, int batch, int L, long long C) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
     float2* buf = lds + kWrSlots;
-    const int G = nbl * batch;
-    const int lid = xcd_remap(blockIdx.x, G);
-    const int bi = lid % nbl, sig = lid / nbl;
-    const BandDev bd = T.bands[T.lists[list_off + bi]];
+    const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
+    const int g = min(it.count, batch - it.s0);
+    if (g <= 0) return;
+    const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
-    const int M = bd.M;
+    const int M = bd.M, n = fd->n;
     const bool blu = bd.chirp >= 0;
-    const float2* Zs = Z + (long long)sig * L;
     const float* w = wt + bd.off;
-    for (int i = threadIdx.x; i < M; i += NT) {
+    const Div dM = mkdiv(M);
+    for (int e = threadIdx.x; e < g * M; e += NT) {
+        int i;
+        const int sg = qdiv(e, dM, i);
+        const float2* Zs = Z + (long long)(it.s0 + sg) * L;
         const int k = bd.k_lo + i;
         const int a = (k == L) ? 0 : k;
         const int bm = (a == 0) ? 0 : L - a;
@@ -232,76 +245,102 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
         int slot = i + bd.rot;
         if (slot >= M) slot -= M;
         if (blu) v = cmul(v, T.chirp[bd.chirp + slot]);
-        buf[slot] = v;
+        buf[lp(sg * n + slot)] = v;
     }
-    if (blu)
-        for (int i = M + threadIdx.x; i < fd->n; i += NT) buf[i] = make_float2(0.f, 0.f);
+    if (blu) {
+        const int pad = n - M;
+        const Div dp = mkdiv(pad);
+        for (int e = threadIdx.x; e < g * pad; e += NT) {
+            int i;
+            const int sg = qdiv(e, dp, i);
+            buf[lp(sg * n + M + i)] = make_float2(0.f, 0.f);
+        }
+    }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
-    float2* cs = coef + (long long)sig * C + bd.off;
-    if (!blu) {
-        for (int i = threadIdx.x; i < M; i += NT) {
-            const float2 v = buf[i];
-            cs[i] = make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
-        }
-    } else {
+    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
+    if (blu) {
         const float2* K = T.kern + bd.kern;
-        for (int i = threadIdx.x; i < fd->n; i += NT) buf[i] = conjf2(cmul(buf[i], K[i]));
-        __syncthreads();
-        lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
-        const float2* ch = T.chirp + bd.chirp;
-        for (int i = threadIdx.x; i < M; i += NT) {
-            // c = conj(ch * conj(D)) / M = conj(ch) D / M
-            const float2 v = cmul(conjf2(ch[i]), buf[i]);
-            cs[i] = cscale(v, bd.inv_M);
+        const Div dn = mkdiv(n);
+        for (int e = threadIdx.x; e < g * n; e += NT) {
+            int i;
+            qdiv(e, dn, i);
+            const int a = lp(e);
+            buf[a] = conjf2(cmul(buf[a], K[i]));
         }
+        __syncthreads();
+        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
+    }
+    const float2* ch = T.chirp + (blu ? bd.chirp : 0);
+    for (int e = threadIdx.x; e < g * M; e += NT) {
+        int i;
+        const int sg = qdiv(e, dM, i);
+        const float2 v = buf[lp(sg * n + i)];
+        float2* cs = coef + (long long)(it.s0 + sg) * C + bd.off;
+        // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
+        cs[i] = blu ? cscale(cmul(conjf2(ch[i]), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
     }
 }
 
 // ----------------------------------------------------------- band synthesis
-// One workgroup per (band, signal): U = F_M c (eq. 10), then the weighted band
+// One workgroup per work item: U = F_M c (eq. 10), then the weighted band
 // spectrum W[off + i] = w_i U[slot(k_lo + i)] in bin order (w = h for S, the
 // T^dagger weight for T^dagger). Overlapping bands are summed later by the
 // owner of each bin.
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __restrict__ coef, float2* __restrict__ W,
-                                                       const float* __restrict__ wt, Tables T, int list_off,
-                                                       int nbl, int batch, long long C) {
+                                                               const float* __restrict__ wt, Tables T, int item0,
+                                                               int nitems, int batch, long long C) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
     float2* buf = lds + kWrSlots;
-    const int G = nbl * batch;
-    const int lid = xcd_remap(blockIdx.x, G);
-    const int bi = lid % nbl, sig = lid / nbl;
-    const BandDev bd = T.bands[T.lists[list_off + bi]];
+    const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
+    const int g = min(it.count, batch - it.s0);
+    if (g <= 0) return;
+    const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
-    const int M = bd.M;
+    const int M = bd.M, n = fd->n;
     const bool blu = bd.chirp >= 0;
-    const float2* cs = coef + (long long)sig * C + bd.off;
     const float2* ch = T.chirp + (blu ? bd.chirp : 0);
-    for (int i = threadIdx.x; i < M; i += NT) {
-        float2 v = cs[i];
+    const Div dM = mkdiv(M);
+    for (int e = threadIdx.x; e < g * M; e += NT) {
+        int i;
+        const int sg = qdiv(e, dM, i);
+        float2 v = coef[(long long)(it.s0 + sg) * C + bd.off + i];
         if (blu) v = cmul(v, ch[i]);
-        buf[i] = v;
+        buf[lp(sg * n + i)] = v;
     }
-    if (blu)
-        for (int i = M + threadIdx.x; i < fd->n; i += NT) buf[i] = make_float2(0.f, 0.f);
+    if (blu) {
+        const int pad = n - M;
+        const Div dp = mkdiv(pad);
+        for (int e = threadIdx.x; e < g * pad; e += NT) {
+            int i;
+            const int sg = qdiv(e, dp, i);
+            buf[lp(sg * n + M + i)] = make_float2(0.f, 0.f);
+        }
+    }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
+    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
     if (blu) {
         const float2* K = T.kern + bd.kern;
-        for (int i = threadIdx.x; i < fd->n; i += NT) buf[i] = conjf2(cmul(buf[i], K[i]));
+        const Div dn = mkdiv(n);
+        for (int e = threadIdx.x; e < g * n; e += NT) {
+            int i;
+            qdiv(e, dn, i);
+            const int a = lp(e);
+            buf[a] = conjf2(cmul(buf[a], K[i]));
+        }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, 1, fd->n, fd, T.tw, wr);
+        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
     }
-    float2* Ws = W + (long long)sig * C + bd.off;
     const float* w = wt + bd.off;
-    for (int i = threadIdx.x; i < M; i += NT) {
+    for (int e = threadIdx.x; e < g * M; e += NT) {
+        int i;
+        const int sg = qdiv(e, dM, i);
         int slot = i + bd.rot;
         if (slot >= M) slot -= M;
-        float2 u = buf[slot];
+        float2 u = buf[lp(sg * n + slot)];
         if (blu) u = cmul(ch[slot], conjf2(u));
-        Ws[i] = cscale(u, w[i]);
+        W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, w[i]);
     }
 }
 

@@ -72,7 +72,7 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iHi = add(h.tw4_hi.data(), h.tw4_hi.size() * sizeof(float));
     const size_t iLo = add(h.tw4_lo.data(), h.tw4_lo.size() * sizeof(float));
     const size_t iWin = add(h.slicewin.data(), h.slicewin.size() * sizeof(float));
-    const size_t iList = add(h.bucket_lists.data(), h.bucket_lists.size() * sizeof(int32_t));
+    const size_t iItems = add(h.items.data(), h.items.size() * sizeof(WorkItem));
     const size_t iWA = add(h.wA.data(), h.wA.size() * sizeof(float));
     const size_t iWS = add(h.wS.data(), h.wS.size() * sizeof(float));
     const size_t iWT = add(h.wT.data(), h.wT.size() * sizeof(float));
@@ -98,7 +98,7 @@ int upload(nsgcqt_plan_s* p) {
     T.tw4_hi = static_cast<const float2*>(at(iHi));
     T.tw4_lo = static_cast<const float2*>(at(iLo));
     T.slicewin = static_cast<const float*>(at(iWin));
-    T.lists = static_cast<const int32_t*>(at(iList));
+    T.items = static_cast<const WorkItem*>(at(iItems));
     p->wA = static_cast<const float*>(at(iWA));
     p->wS = static_cast<const float*>(at(iWS));
     p->wT = static_cast<const float*>(at(iWT));
@@ -138,7 +138,7 @@ Pass pass_b(const HostPlan& h) {
     return q;
 }
 
-int lds_pass(const Pass& q) { return (kWrSlots + q.tile * q.ld) * static_cast<int>(sizeof(float2)); }
+int lds_pass(const Pass& q) { return (kWrSlots + lds_slots(q.tile * q.ld)) * static_cast<int>(sizeof(float2)); }
 
 #define DISPATCH_NT(nt, KERNEL, ...)                                                         \
     switch (nt) {                                                                            \
@@ -199,17 +199,16 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
               hipStream_t s) {
     const HostPlan& h = p->h;
     for (const auto& bk : h.buckets) {
-        const int nbl = static_cast<int>(bk.bands.size());
-        const int lds = (kWrSlots + bk.max_work) * static_cast<int>(sizeof(float2));
-        const dim3 grid(nbl * batch), block(bk.nt);
+        const int lds = (kWrSlots + lds_slots(bk.lds_elems)) * static_cast<int>(sizeof(float2));
+        const dim3 grid(bk.nitems), block(bk.nt);
         auto go = [&](auto ka, auto ks) -> int {
             if (analysis) {
                 if (int r = launch_prep(ka, lds)) return r;
-                hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, wt, p->T, bk.list_off, nbl, batch,
+                hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
                                    static_cast<int>(h.L), static_cast<long long>(h.C));
             } else {
                 if (int r = launch_prep(ks, lds)) return r;
-                hipLaunchKernelGGL(ks, grid, block, lds, s, in, out, wt, p->T, bk.list_off, nbl, batch,
+                hipLaunchKernelGGL(ks, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
                                    static_cast<long long>(h.C));
             }
             HIP_TRY(hipGetLastError());

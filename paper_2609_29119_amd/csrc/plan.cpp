@@ -306,8 +306,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         f.tile_b = static_cast<int>(std::min<int64_t>(f.tile_b, f.L1));
         f.ld_a = static_cast<int>(f.L1 | 1);
         f.ld_b = static_cast<int>(f.L2 | 1);
-        if (static_cast<int64_t>(f.tile_a) * f.ld_a * 8 > 160 * 1024 - 1024 ||
-            static_cast<int64_t>(f.tile_b) * f.ld_b * 8 > 160 * 1024 - 1024)
+        if (static_cast<int64_t>(lds_slots(f.tile_a * f.ld_a)) * 8 > 160 * 1024 - 1024 ||
+            static_cast<int64_t>(lds_slots(f.tile_b * f.ld_b)) * 8 > 160 * 1024 - 1024)
             return fail(err, NSGCQT_EUNSUPPORTED, "four-step tile exceeds LDS");
         int64_t s = 1;
         while (s * s < L) ++s;
@@ -388,10 +388,21 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     p.buckets.erase(std::remove_if(p.buckets.begin(), p.buckets.end(),
                                    [](const Bucket& b) { return b.bands.empty(); }),
                     p.buckets.end());
-    p.bucket_lists.clear();
+    // one work item per (band, group of signals): small transforms of one band
+    // for several signals share a workgroup, up to nt * ept elements
+    p.items.clear();
     for (auto& bk : p.buckets) {
-        bk.list_off = static_cast<int>(p.bucket_lists.size());
-        p.bucket_lists.insert(p.bucket_lists.end(), bk.bands.begin(), bk.bands.end());
+        bk.item_off = static_cast<int>(p.items.size());
+        const int E = bk.nt * bk.ept;
+        bk.lds_elems = 0;
+        for (int32_t l : bk.bands) {
+            const int n = work[l];
+            const int G = std::max(1, std::min(batch, E / n));
+            bk.lds_elems = std::max(bk.lds_elems, G * n);
+            for (int s0 = 0; s0 < batch; s0 += G)
+                p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), 0});
+        }
+        bk.nitems = static_cast<int>(p.items.size()) - bk.item_off;
     }
 
     // ---- slicing window (Sec. 4): zero, sin^2 rise, flat, cos^2 fall, zero

@@ -25,7 +25,9 @@ struct Bucket {
     int max_work;         // largest transform length in the bucket
     int64_t coeffs;       // sum of M over its bands
     std::vector<int32_t> bands;
-    int list_off;         // offset of its band list in the device list array
+    int item_off;         // first work item of the bucket in HostPlan::items
+    int nitems;
+    int lds_elems;        // largest count * transform length over its items
 };
 
 // Four-step split of the packed FFT: L = L1 * L2. Pass A transforms columns
@@ -67,7 +69,7 @@ struct HostPlan {
     std::vector<float> chirp, kern;         // Bluestein tables
     std::vector<float> slicewin;            // sliced plans: window of length N
     std::vector<Bucket> buckets;
-    std::vector<int32_t> bucket_lists;
+    std::vector<WorkItem> items;
     FourStep fs4{};
 
     int64_t ws_an = 0, ws_syn = 0;

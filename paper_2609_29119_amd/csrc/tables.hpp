@@ -35,4 +35,15 @@ struct BandDev {
     float inv_M;
 };
 
+// One workgroup of a band kernel: band `band` for signals s0 .. s0 + count - 1.
+struct WorkItem {
+    int32_t band;
+    int32_t s0;
+    int32_t count;
+    int32_t pad;
+};
+
+// LDS slots holding n complex values under the padded index i + i/8.
+inline int lds_slots(int n) { return n + (n > 0 ? (n - 1) / 8 : 0) + 1; }
+
 }  // namespace nsg
