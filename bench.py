@@ -96,6 +96,90 @@ def cpu_baseline(w, x, target_s=12.0):
             "host_cpus": len(os.sched_getaffinity(0))}
 
 
+# HIP kernel (rocprofv3 name) -> stage name reported by nsgcqt_stage_info
+def stage_of_kernel(name):
+    import re
+    m = re.search(r"k_(fwd_a|inv_a|pass_b|band_analysis|band_synthesis)<(\d+), (\d+)(?:, (true|false))?>", name)
+    if not m:
+        return None
+    k, nt, ept, inv = m.groups()
+    if k == "fwd_a":
+        return "fft_fwd_a"
+    if k == "inv_a":
+        return "fft_inv_a_overlap_add"
+    if k == "pass_b":
+        return "fft_inv_b" if inv == "true" else "fft_fwd_b"
+    return f"{k}_{nt}x{ept}"
+
+
+def summarize_profile(trace_dir, fetch_dir, write_dir, workload, command, calib_bytes):
+    """Per-kernel durations (kernel trace) and HBM bytes (FETCH_SIZE /
+    WRITE_SIZE, KiB per dispatch) scaled by the same counters read on a
+    device copy of calib_bytes bytes. Writes profiles/ summaries."""
+    import csv
+    import glob
+    import statistics
+
+    def rows(d, suffix):
+        f = glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
+        return list(csv.DictReader(open(f[0]))) if f else []
+
+    stats = rows(trace_dir, "kernel_stats.csv")
+    lines = [f"# Kernel trace: {workload} round trip", "", "Command:", "", "```", command["trace"], "```", "",
+             "| kernel | stage | calls | avg us | min us | max us | share % |", "|---|---|---|---|---|---|---|"]
+    for r in stats:
+        st = stage_of_kernel(r["Name"]) or "-"
+        short = r["Name"].split("(")[0].replace("nsg::", "")
+        lines.append(f"| `{short}` | {st} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    out = {"workload": workload, "source_hash": kernel_source_hash(), "commands": command, "kernels": {}}
+    per = {}
+    for d, cname in ((fetch_dir, "FETCH_SIZE"), (write_dir, "WRITE_SIZE")):
+        for r in rows(d, "counter_collection.csv"):
+            if r["Counter_Name"] != cname:
+                continue
+            per.setdefault(r["Kernel_Name"], {}).setdefault(cname, []).append(float(r["Counter_Value"]))
+    copy = [v for k, v in per.items() if "copy" in k.lower()]
+    calib = None
+
+    def top(vals):
+        # the calibration copies are the largest copy dispatches of the run
+        vals = [x for x in vals if x > 0]
+        if not vals:
+            return 0.0
+        m = max(vals)
+        return statistics.median([x for x in vals if x >= 0.9 * m])
+
+    if copy and calib_bytes:
+        f = top([x for c in copy for x in c.get("FETCH_SIZE", [])])
+        w = top([x for c in copy for x in c.get("WRITE_SIZE", [])])
+        calib = {"bytes": calib_bytes, "fetch_kib": f, "write_kib": w,
+                 "fetch_factor": calib_bytes / 1024.0 / f if f else None,
+                 "write_factor": calib_bytes / 1024.0 / w if w else None}
+    out["copy_calibration"] = calib
+    lines += ["", f"# HBM traffic per launch ({workload})", "", "Commands:", "", "```", command.get("fetch", ""),
+              command.get("write", ""), "```", "",
+              f"Copy calibration: {json.dumps(calib)}", "",
+              "| stage | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes / launch (scaled) |", "|---|---|---|---|"]
+    for k, c in per.items():
+        st = stage_of_kernel(k)
+        if not st:
+            continue
+        f = statistics.median(c.get("FETCH_SIZE", [float("nan")]))
+        w = statistics.median(c.get("WRITE_SIZE", [float("nan")]))
+        hb = None
+        if calib and calib["fetch_factor"] and calib["write_factor"]:
+            hb = f * 1024.0 * calib["fetch_factor"] + w * 1024.0 * calib["write_factor"]
+        out["kernels"][st] = {"fetch_kib": f, "write_kib": w, "hbm_bytes_per_launch": hb}
+        lines.append(f"| {st} | {f:.0f} | {w:.0f} | {hb if hb is None else f'{hb:.4g}'} |")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"traffic_{workload}.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+    with open(os.path.join(ROOT, "profiles", f"roundtrip_{workload}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -105,7 +189,16 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-stage-events", action="store_true",
                     help="time the loop without per-kernel events (for profiler runs)")
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="after timing, run device copies of this many MiB (counter calibration)")
+    ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="summarise rocprofv3 outputs into profiles/ and exit")
+    ap.add_argument("--commands", default="{}", help="JSON of the profiler commands (for the summary)")
     args = ap.parse_args()
+    if args.summarize_profile:
+        summarize_profile(*args.summarize_profile, args.workload, json.loads(args.commands),
+                          args.copy_calib_mb * 1024 * 1024)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; a batch shards across GPUs with no "
                           "communication, so --gpus must be 1"}))
@@ -176,6 +269,14 @@ def main():
             stages.append({"kernel": n_, "ms": round(float(d_), 5), "alg_bytes": b_,
                            "GBps": round(b_ / (d_ * 1e-3) / 1e9, 1)})
         ev.close()
+
+    if args.copy_calib_mb:
+        src = torch.empty(args.copy_calib_mb * 1024 * 1024 // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # accuracy of this run's round trip (GPU result against the input)
     xr_np = xr.cpu().numpy().astype(np.float64)

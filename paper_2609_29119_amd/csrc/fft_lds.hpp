@@ -162,11 +162,22 @@ struct Div {
 __device__ __forceinline__ Div mkdiv(int d) { return Div{1.0f / static_cast<float>(d), d}; }
 __device__ __forceinline__ int qdiv(int x, Div v, int& rem) {
     int q = static_cast<int>(static_cast<float>(x) * v.r);
-    int r = x - q * v.d;
+    int r = x - __mul24(q, v.d);
     if (r < 0) { --q; r += v.d; }
     else if (r >= v.d) { ++q; r -= v.d; }
     rem = r;
     return q;
+}
+
+// Stage twiddle omega_n^t from the two-level table in LDS: hi values at
+// twl[0 .. nhi), lo values at twl[nhi .. nhi + 2^lg).
+struct TwL {
+    const float2* t;
+    int nhi;
+    int lg;
+};
+__device__ __forceinline__ float2 tw_at(const TwL& w, int t) {
+    return cmul(w.t[t >> w.lg], w.t[w.nhi + (t & ((1 << w.lg) - 1))]);
 }
 
 // Odd prime radix with the symmetric pairing of DftOdd; cos/sin of 2 pi u/R
@@ -224,11 +235,11 @@ template <> struct Radix<13> { __device__ __forceinline__ static void run(float2
 // the length-R DFT, and after a barrier writes out[(jj - k) R + k + r Ns].
 template <int R, int NT, int EPT>
 __device__ __forceinline__ void stage_fixed(float2* buf, int nb, int ld, int n, int Ns,
-                                            const float2* __restrict__ tw) {
+                                            const float2* __restrict__ tw, const TwL& twl) {
     constexpr int BPT = (EPT + R - 1) / R;
     const int tid = stage_tid();
     const int m = n / R;
-    const int total = nb * m;
+    const int total = __mul24(nb, m);
     const int stride = n / (Ns * R);
     const Div dm = mkdiv(m), dns = mkdiv(Ns);
     float2 v[BPT][R];
@@ -238,26 +249,39 @@ __device__ __forceinline__ void stage_fixed(float2* buf, int nb, int ld, int n, 
         const int j = tid + b * NT;
         ob[b] = -1;
         if (j < total) {
-            int jj, k;
-            const int t = qdiv(j, dm, jj);
-            qdiv(jj, dns, k);
-            const int src = t * ld + jj;
+            int jj = j, t = 0, k = 0;
+            if (nb > 1) t = qdiv(j, dm, jj);
+            if (Ns > 1) qdiv(jj, dns, k);
+            const int base = __mul24(t, ld);
+            int a = base + jj;
 #pragma unroll
-            for (int r = 0; r < R; ++r) v[b][r] = buf[lp(src + r * m)];
+            for (int r = 0; r < R; ++r) {
+                v[b][r] = buf[lp(a)];
+                a += m;
+            }
             if (Ns > 1) {
+                const int step = __mul24(k, stride);
+                int ti = step;
 #pragma unroll
-                for (int r = 1; r < R; ++r) v[b][r] = cmul(v[b][r], tw[r * k * stride]);
+                for (int r = 1; r < R; ++r) {
+                    v[b][r] = cmul(v[b][r], tw_at(twl, ti));
+                    ti += step;
+                }
             }
             Radix<R>::run(v[b], tw, m);
-            ob[b] = t * ld + (jj - k) * R + k;
+            ob[b] = base + (jj - k) * R + k;
         }
     }
     __syncthreads();
 #pragma unroll
     for (int b = 0; b < BPT; ++b) {
         if (ob[b] >= 0) {
+            int a = ob[b];
 #pragma unroll
-            for (int r = 0; r < R; ++r) buf[lp(ob[b] + r * Ns)] = v[b][r];
+            for (int r = 0; r < R; ++r) {
+                buf[lp(a)] = v[b][r];
+                a += Ns;
+            }
         }
     }
     __syncthreads();
@@ -269,7 +293,7 @@ __device__ __forceinline__ void stage_fixed(float2* buf, int nb, int ld, int n, 
 // the symmetric sums of DftOdd, reading the twiddled inputs from LDS.
 template <int NT, int EPT>
 __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n, int Ns, int R,
-                                              const float2* __restrict__ tw, float2* wr) {
+                                              const float2* __restrict__ tw, const TwL& twl, float2* wr) {
     constexpr int IPT = (EPT * 6 + 9) / 10;   // items <= nb n (R+1)/(2R) <= 0.55 NT EPT
     const int tid = stage_tid();
     const int m = n / R;
@@ -278,15 +302,15 @@ __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n
     const Div dn = mkdiv(n), dm = mkdiv(m), dns = mkdiv(Ns), dhp = mkdiv(h + 1);
     for (int t = tid; t < R; t += NT) wr[t] = tw[t * m];   // omega_R^t
     if (Ns > 1) {
-        const int tot = nb * n;
+        const int tot = __mul24(nb, n);
         for (int e = tid; e < tot; e += NT) {
-            int i, jj, k;
-            const int t = qdiv(e, dn, i);
+            int i = e, jj, k, t = 0;
+            if (nb > 1) t = qdiv(e, dn, i);
             const int r = qdiv(i, dm, jj);
             if (r) {
                 qdiv(jj, dns, k);
-                const int a = lp(t * ld + i);
-                buf[a] = cmul(buf[a], tw[r * k * stride]);
+                const int a = lp(__mul24(t, ld) + i);
+                buf[a] = cmul(buf[a], tw_at(twl, __mul24(__mul24(r, k), stride)));
             }
         }
     }
@@ -300,17 +324,21 @@ __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n
         const int it = tid + b * NT;
         ob[b] = -1;
         if (it < items) {
-            int q, jj, k;
+            int q, jj, k = 0, t = 0;
             const int j = qdiv(it, dhp, q);
-            const int t = qdiv(j, dm, jj);
-            qdiv(jj, dns, k);
-            const int src = t * ld + jj;
+            jj = j;
+            if (nb > 1) t = qdiv(j, dm, jj);
+            if (Ns > 1) qdiv(jj, dns, k);
+            const int src = __mul24(t, ld) + jj;
             float2 A = buf[lp(src)], B = make_float2(0.f, 0.f);
             int idx = 0;
+            int ia = src, ic = src + __mul24(R, m);
             for (int r = 1; r <= h; ++r) {
                 idx += q;
                 if (idx >= R) idx -= R;
-                const float2 a = buf[lp(src + r * m)], c = buf[lp(src + (R - r) * m)];
+                ia += m;
+                ic -= m;
+                const float2 a = buf[lp(ia)], c = buf[lp(ic)];
                 const float2 w = wr[idx];        // (cos, -sin) of 2 pi idx / R
                 A.x += (a.x + c.x) * w.x;
                 A.y += (a.y + c.y) * w.x;
@@ -319,7 +347,7 @@ __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n
             }
             o0[b] = make_float2(A.x + B.y, A.y - B.x);
             o1[b] = make_float2(A.x - B.y, A.y + B.x);
-            ob[b] = t * ld + (jj - k) * R + k;
+            ob[b] = __mul24(t, ld) + __mul24(jj - k, R) + k;
             oq[b] = q;
         }
     }
@@ -327,35 +355,39 @@ __device__ __forceinline__ void stage_generic(float2* buf, int nb, int ld, int n
 #pragma unroll
     for (int b = 0; b < IPT; ++b) {
         if (ob[b] >= 0) {
-            buf[lp(ob[b] + oq[b] * Ns)] = o0[b];
-            if (oq[b]) buf[lp(ob[b] + (R - oq[b]) * Ns)] = o1[b];
+            buf[lp(ob[b] + __mul24(oq[b], Ns))] = o0[b];
+            if (oq[b]) buf[lp(ob[b] + __mul24(R - oq[b], Ns))] = o1[b];
         }
     }
     __syncthreads();
 }
 
 // Forward DFTs of nb sequences of length d->n at LDS slots lp(t*ld + i). `wr`
-// is LDS scratch for kGenericMaxRadix complex values. Ends with a barrier
-// (when there is at least one stage).
+// is LDS scratch for kGenericMaxRadix complex values and `twlds` for kTwSlots.
+// Ends with a barrier (when there is at least one stage).
 template <int NT, int EPT>
 __device__ __forceinline__ void lds_fft(float2* buf, int nb, int ld, const FftDesc* __restrict__ d,
-                                        const float2* __restrict__ twpool, float2* wr) {
+                                        const float2* __restrict__ twpool, float2* wr, float2* twlds) {
     const int n = d->n;
     const int ns = d->nstages;
     const float2* tw = twpool + d->tw;
+    // the first stage (Ns = 1) needs no twiddles and ends with a barrier, so
+    // the table is visible from the second stage on
+    const TwL twl{twlds, d->nhi, d->lg};
+    for (int i = threadIdx.x; i < d->nhi + (1 << d->lg); i += NT) twlds[i] = tw[n + i];
     int Ns = 1;
     for (int s = 0; s < ns; ++s) {
         const int R = d->radix[s];
         switch (R) {
-            case 8: stage_fixed<8, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 4: stage_fixed<4, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 2: stage_fixed<2, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 3: stage_fixed<3, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 5: stage_fixed<5, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 7: stage_fixed<7, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 11: stage_fixed<11, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            case 13: stage_fixed<13, NT, EPT>(buf, nb, ld, n, Ns, tw); break;
-            default: stage_generic<NT, EPT>(buf, nb, ld, n, Ns, R, tw, wr); break;
+            case 8: stage_fixed<8, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 4: stage_fixed<4, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 2: stage_fixed<2, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 3: stage_fixed<3, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 5: stage_fixed<5, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 7: stage_fixed<7, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 11: stage_fixed<11, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            case 13: stage_fixed<13, NT, EPT>(buf, nb, ld, n, Ns, tw, twl); break;
+            default: stage_generic<NT, EPT>(buf, nb, ld, n, Ns, R, tw, twl, wr); break;
         }
         Ns *= R;
     }

@@ -14,6 +14,7 @@
 namespace nsg {
 
 constexpr int kWrSlots = 64;   // LDS complex slots reserved for a generic radix table
+static_assert(kGenericMaxRadix <= kWrSlots, "generic radix table exceeds its LDS slots");
 
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
 // caps each kernel at 256 VGPRs per lane.
@@ -40,7 +41,8 @@ struct Pass {
     int ntile;
     int ld;
     int fft;                 // FftDesc index of the pass length
-    int split;               // four-step twiddle split
+    int split;               // four-step twiddles: hi[t >> split] * lo[t & (2^split - 1)]
+    int nhi4;                // number of hi values
     int L;
 };
 
@@ -60,8 +62,24 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
     return x * q + (x < r ? x : r) + i;
 }
 
-__device__ __forceinline__ float2 tw4(const Tables& T, int t, int split) {
-    return cmul(T.tw4_hi[t / split], T.tw4_lo[t % split]);
+// LDS layout of the pass kernels: generic radix table, FFT twiddles, the
+// four-step twiddles (hi then lo) and the data.
+__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, float2*& wr, float2*& twl, float2*& t4,
+                                         float2*& buf) {
+    wr = lds;
+    twl = lds + kWrSlots;
+    t4 = twl + kTwSlots;
+    buf = t4 + p.nhi4 + (1 << p.split);
+}
+
+template <int NT>
+__device__ __forceinline__ void load_tw4(float2* t4, const Pass& p, const Tables& T) {
+    for (int i = threadIdx.x; i < p.nhi4; i += NT) t4[i] = T.tw4_hi[i];
+    for (int i = threadIdx.x; i < (1 << p.split); i += NT) t4[p.nhi4 + i] = T.tw4_lo[i];
+}
+
+__device__ __forceinline__ float2 tw4(const float2* t4, const Pass& p, int t) {
+    return cmul(t4[t >> p.split], t4[p.nhi4 + (t & ((1 << p.split) - 1))]);
 }
 
 // -------------------------------------------------- packed FFT, pass A (columns)
@@ -72,8 +90,9 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
                                                       Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
     extern __shared__ float2 lds[];
-    float2* wr = lds;
-    float2* buf = lds + kWrSlots;
+    float2 *wr, *twl, *t4, *buf;
+    pass_lds(lds, p, wr, twl, t4, buf);
+    load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
@@ -86,7 +105,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
         for (int e = threadIdx.x; e < tot; e += NT) {
             int c;
             const int n1 = qdiv(e, dc, c);
-            buf[lp(c * p.ld + n1)] = z[(long long)n1 * p.L2 + n2a + c];
+            buf[lp(__mul24(c, p.ld) + n1)] = z[__mul24(n1, p.L2) + n2a + c];
         }
     } else {
         // padded coordinate of sample 2j of slice s is s H + 2j; the signal
@@ -99,17 +118,18 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
             const long long t = base + 2 * j;
             const float v0 = (t >= 0 && t < sl.n) ? x[t] : 0.f;
             const float v1 = (t + 1 >= 0 && t + 1 < sl.n) ? x[t + 1] : 0.f;
-            buf[lp(c * p.ld + n1)] = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
+            buf[lp(__mul24(c, p.ld) + n1)] = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
         }
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr);
+    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr, twl);
+    __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
         int c;
         const int k1 = qdiv(e, dc, c);
         const int n2 = n2a + c;
-        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[lp(c * p.ld + k1)], tw4(T, n2 * k1, p.split));
+        Ys[__mul24(k1, p.L2) + n2] = cmul(buf[lp(__mul24(c, p.ld) + k1)], tw4(t4, p, __mul24(n2, k1)));
     }
 }
 
@@ -132,8 +152,9 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
                                                       Pass p, Tables T, int batch, long long C) {
     extern __shared__ float2 lds[];
-    float2* wr = lds;
-    float2* buf = lds + kWrSlots;
+    float2 *wr, *twl, *t4, *buf;
+    pass_lds(lds, p, wr, twl, t4, buf);
+    load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
@@ -145,7 +166,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     for (int e = threadIdx.x; e < tot; e += NT) {
         int c;
         const int n1 = qdiv(e, dc, c);
-        const int q = n1 * p.L2 + n2a + c;
+        const int q = __mul24(n1, p.L2) + n2a + c;
         float2 xq = gather_bin(T, Ws, q);
         float2 xm = gather_bin(T, Ws, p.L - q);
         if (q == 0) { xq.y = 0.f; xm.y = 0.f; }
@@ -153,16 +174,17 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
         const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w)
         const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
         const float2 zq = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
-        buf[lp(c * p.ld + n1)] = make_float2(0.5f * zq.x, -0.5f * zq.y);   // conj(Z_q)
+        buf[lp(__mul24(c, p.ld) + n1)] = make_float2(0.5f * zq.x, -0.5f * zq.y);   // conj(Z_q)
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr);
+    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr, twl);
+    __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
         int c;
         const int k1 = qdiv(e, dc, c);
         const int n2 = n2a + c;
-        Ys[(long long)k1 * p.L2 + n2] = cmul(buf[lp(c * p.ld + k1)], tw4(T, n2 * k1, p.split));
+        Ys[__mul24(k1, p.L2) + n2] = cmul(buf[lp(__mul24(c, p.ld) + k1)], tw4(t4, p, __mul24(n2, k1)));
     }
 }
 
@@ -175,8 +197,9 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
                                                        Pass p, Tables T, int batch, long long out_stride,
                                                        float inv_L) {
     extern __shared__ float2 lds[];
-    float2* wr = lds;
-    float2* buf = lds + kWrSlots;
+    float2 *wr, *twl, *t4, *buf;
+    pass_lds(lds, p, wr, twl, t4, buf);
+    load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
@@ -188,16 +211,16 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
     for (int e = threadIdx.x; e < tot; e += NT) {
         int n2;
         const int r = qdiv(e, dl2, n2);
-        buf[lp(r * p.ld + n2)] = Ys[e];
+        buf[lp(__mul24(r, p.ld) + n2)] = Ys[e];
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, rows, p.ld, T.ffts + p.fft, T.tw, wr);
+    lds_fft<NT, EPT>(buf, rows, p.ld, T.ffts + p.fft, T.tw, wr, twl);
     float2* os = out + (long long)sig * out_stride;
     for (int e = threadIdx.x; e < tot; e += NT) {
         int r;
         const int k2 = qdiv(e, drows, r);
-        const long long k = (long long)k1a + r + (long long)p.L1 * k2;
-        const float2 v = buf[lp(r * p.ld + k2)];
+        const int k = k1a + r + __mul24(p.L1, k2);
+        const float2 v = buf[lp(__mul24(r, p.ld) + k2)];
         os[k] = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
     }
 }
@@ -218,7 +241,8 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
                                                               int nitems, int batch, int L, long long C) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
-    float2* buf = lds + kWrSlots;
+    float2* twl = lds + kWrSlots;
+    float2* buf = twl + kTwSlots;
     const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
@@ -245,7 +269,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
         int slot = i + bd.rot;
         if (slot >= M) slot -= M;
         if (blu) v = cmul(v, T.chirp[bd.chirp + slot]);
-        buf[lp(sg * n + slot)] = v;
+        buf[lp(__mul24(sg, n) + slot)] = v;
     }
     if (blu) {
         const int pad = n - M;
@@ -253,11 +277,11 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
         for (int e = threadIdx.x; e < g * pad; e += NT) {
             int i;
             const int sg = qdiv(e, dp, i);
-            buf[lp(sg * n + M + i)] = make_float2(0.f, 0.f);
+            buf[lp(__mul24(sg, n) + M + i)] = make_float2(0.f, 0.f);
         }
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
+    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
     if (blu) {
         const float2* K = T.kern + bd.kern;
         const Div dn = mkdiv(n);
@@ -268,13 +292,13 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
             buf[a] = conjf2(cmul(buf[a], K[i]));
         }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
+        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
     }
     const float2* ch = T.chirp + (blu ? bd.chirp : 0);
     for (int e = threadIdx.x; e < g * M; e += NT) {
         int i;
         const int sg = qdiv(e, dM, i);
-        const float2 v = buf[lp(sg * n + i)];
+        const float2 v = buf[lp(__mul24(sg, n) + i)];
         float2* cs = coef + (long long)(it.s0 + sg) * C + bd.off;
         // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
         cs[i] = blu ? cscale(cmul(conjf2(ch[i]), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
@@ -292,7 +316,8 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
                                                                int nitems, int batch, long long C) {
     extern __shared__ float2 lds[];
     float2* wr = lds;
-    float2* buf = lds + kWrSlots;
+    float2* twl = lds + kWrSlots;
+    float2* buf = twl + kTwSlots;
     const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
@@ -307,7 +332,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
         const int sg = qdiv(e, dM, i);
         float2 v = coef[(long long)(it.s0 + sg) * C + bd.off + i];
         if (blu) v = cmul(v, ch[i]);
-        buf[lp(sg * n + i)] = v;
+        buf[lp(__mul24(sg, n) + i)] = v;
     }
     if (blu) {
         const int pad = n - M;
@@ -315,11 +340,11 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
         for (int e = threadIdx.x; e < g * pad; e += NT) {
             int i;
             const int sg = qdiv(e, dp, i);
-            buf[lp(sg * n + M + i)] = make_float2(0.f, 0.f);
+            buf[lp(__mul24(sg, n) + M + i)] = make_float2(0.f, 0.f);
         }
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
+    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
     if (blu) {
         const float2* K = T.kern + bd.kern;
         const Div dn = mkdiv(n);
@@ -330,7 +355,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
             buf[a] = conjf2(cmul(buf[a], K[i]));
         }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr);
+        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
     }
     const float* w = wt + bd.off;
     for (int e = threadIdx.x; e < g * M; e += NT) {
@@ -338,7 +363,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
         const int sg = qdiv(e, dM, i);
         int slot = i + bd.rot;
         if (slot >= M) slot -= M;
-        float2 u = buf[lp(sg * n + slot)];
+        float2 u = buf[lp(__mul24(sg, n) + slot)];
         if (blu) u = cmul(ch[slot], conjf2(u));
         W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, w[i]);
     }

@@ -127,6 +127,7 @@ Pass pass_a(const HostPlan& h) {
     q.ntile = static_cast<int>((h.fs4.L2 + q.tile - 1) / q.tile);
     q.ld = h.fs4.ld_a; q.fft = h.fs4.fft1;
     q.split = static_cast<int>(h.fs4.split); q.L = static_cast<int>(h.L);
+    q.nhi4 = static_cast<int>(h.tw4_hi.size() / 2);
     return q;
 }
 
@@ -138,7 +139,9 @@ Pass pass_b(const HostPlan& h) {
     return q;
 }
 
-int lds_pass(const Pass& q) { return (kWrSlots + lds_slots(q.tile * q.ld)) * static_cast<int>(sizeof(float2)); }
+int lds_pass(const Pass& q) {
+    return (kWrSlots + kTwSlots + q.nhi4 + (1 << q.split) + lds_slots(q.tile * q.ld)) * static_cast<int>(sizeof(float2));
+}
 
 #define DISPATCH_NT(nt, KERNEL, ...)                                                         \
     switch (nt) {                                                                            \
@@ -199,7 +202,7 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
               hipStream_t s) {
     const HostPlan& h = p->h;
     for (const auto& bk : h.buckets) {
-        const int lds = (kWrSlots + lds_slots(bk.lds_elems)) * static_cast<int>(sizeof(float2));
+        const int lds = (kWrSlots + kTwSlots + lds_slots(bk.lds_elems)) * static_cast<int>(sizeof(float2));
         const dim3 grid(bk.nitems), block(bk.nt);
         auto go = [&](auto ka, auto ks) -> int {
             if (analysis) {
@@ -217,8 +220,9 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
         };
         int r = NSGCQT_OK;
         if (bk.nt == 64) r = go(k_band_analysis<64, 8>, k_band_synthesis<64, 8>);
-        else if (bk.nt == 256) r = go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
-        else if (bk.ept == 8) r = go(k_band_analysis<1024, 8>, k_band_synthesis<1024, 8>);
+        else if (bk.nt == 256 && bk.ept == 8) r = go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
+        else if (bk.nt == 256) r = go(k_band_analysis<256, 16>, k_band_synthesis<256, 16>);
+        else if (bk.nt == 512) r = go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
         else r = go(k_band_analysis<1024, 16>, k_band_synthesis<1024, 16>);
         if (r) return r;
     }
@@ -492,11 +496,13 @@ int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, doub
         st.push_back({"fft_fwd_b", 16.0 * L * b});
         for (const auto& bk : h.buckets) {
             const double cb = static_cast<double>(bk.coeffs);
-            st.push_back({"band_analysis_" + std::to_string(bk.nt), (cb / C * 8.0 * L + 8.0 * cb) * b});
+            st.push_back({"band_analysis_" + std::to_string(bk.nt) + "x" + std::to_string(bk.ept),
+                          (cb / C * 8.0 * L + 8.0 * cb) * b});
         }
     } else {
         for (const auto& bk : h.buckets)
-            st.push_back({"band_synthesis_" + std::to_string(bk.nt), 16.0 * static_cast<double>(bk.coeffs) * b});
+            st.push_back({"band_synthesis_" + std::to_string(bk.nt) + "x" + std::to_string(bk.ept),
+                          16.0 * static_cast<double>(bk.coeffs) * b});
         st.push_back({"fft_inv_a_overlap_add", (8.0 * C + 8.0 * L) * b});
         st.push_back({"fft_inv_b", 16.0 * L * b});
     }

@@ -118,6 +118,13 @@ struct FftRegistry {
             if (rad[s] > 8) d.max_generic = std::max(d.max_generic, rad[s]);
         }
         for (int64_t t = 0; t < n; ++t) push_c(p.twpool, root(t, n));
+        int lg = 0;
+        while ((int64_t(1) << (2 * lg)) < n) ++lg;
+        d.lg = lg;
+        d.nhi = static_cast<int32_t>((n + (int64_t(1) << lg) - 1) >> lg);
+        for (int64_t i = 0; i < d.nhi; ++i) push_c(p.twpool, root(i << lg, n));
+        for (int64_t j = 0; j < (int64_t(1) << lg); ++j) push_c(p.twpool, root(j, n));
+        if (d.nhi + (1 << lg) > kTwSlots) return -1;
         p.ffts.push_back(d);
         const int id = static_cast<int>(p.ffts.size()) - 1;
         index[n] = id;
@@ -309,9 +316,10 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         if (static_cast<int64_t>(lds_slots(f.tile_a * f.ld_a)) * 8 > 160 * 1024 - 1024 ||
             static_cast<int64_t>(lds_slots(f.tile_b * f.ld_b)) * 8 > 160 * 1024 - 1024)
             return fail(err, NSGCQT_EUNSUPPORTED, "four-step tile exceeds LDS");
-        int64_t s = 1;
-        while (s * s < L) ++s;
-        f.split = s;
+        int lg = 0;
+        while ((int64_t(1) << (2 * lg)) < L) ++lg;
+        const int64_t s = int64_t(1) << lg;
+        f.split = lg;
         p.tw4_hi.clear(); p.tw4_lo.clear();
         for (int64_t i = 0; i * s < L; ++i) push_c(p.tw4_hi, root(i * s, L));
         for (int64_t j = 0; j < s; ++j) push_c(p.tw4_lo, root(j, L));
@@ -364,7 +372,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
 
     // ---- buckets by transform length
     struct Tier { int max_work, nt, ept; };
-    const Tier tiers[] = {{512, 64, 8}, {2048, 256, 8}, {8192, 1024, 8}, {16384, 1024, 16}};
+    const Tier tiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}, {16384, 1024, 16}};
     p.buckets.clear();
     for (const auto& t : tiers) {
         Bucket bk{};
@@ -373,7 +381,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     }
     for (size_t l = 0; l < p.bands.size(); ++l) {
         int ti = -1;
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 5; ++i)
             if (work[l] <= tiers[i].max_work) { ti = i; break; }
         if (ti < 0)
             return fail(err, NSGCQT_EUNSUPPORTED,

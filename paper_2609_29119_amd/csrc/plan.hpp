@@ -39,7 +39,7 @@ struct FourStep {
     int tile_a, tile_b;
     int nt_a, nt_b;       // threads per workgroup of each pass
     int ld_a, ld_b;       // LDS leading dimensions (padded)
-    int64_t split;        // omega_L^t = hi[t / split] * lo[t % split]
+    int64_t split;        // omega_L^t = hi[t >> split] * lo[t & (2^split - 1)]
 };
 
 struct HostPlan {

@@ -20,8 +20,15 @@ struct FftDesc {
     int32_t nstages;
     int32_t tw;
     int32_t max_generic;     // largest generic (odd prime >= 11) radix, 0 if none
+    // two-level twiddles: omega_n^t = hi[t >> lg] * lo[t & (2^lg - 1)], with
+    // hi at tw + n (ceil(n / 2^lg) values) and lo right after it (2^lg values)
+    int32_t lg;
+    int32_t nhi;
     int16_t radix[kMaxStages];
 };
+
+// LDS slots reserved for the two-level twiddles of any length up to 16384.
+constexpr int kTwSlots = 288;
 
 // One band of the layout as the band kernels see it.
 struct BandDev {
