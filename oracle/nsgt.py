@@ -99,6 +99,22 @@ def analyse(lay: Layout, x, mode: str = "direct") -> np.ndarray:
     return c.reshape(*lead, lay.n_coeffs)
 
 
+def analyse_bands(lay: Layout, x, bands, mode: str = "direct") -> dict:
+    """Coefficients of the listed bands only: {band index: [..., M]}.
+
+    The same definition as ``analyse`` restricted to a subset of bands, for
+    checking sampled outputs of large transforms one band at a time."""
+    xb, lead = _as_batch(np.asarray(x, dtype=np.float64), lay.N)
+    X = np.fft.fft(xb, axis=-1)
+    out = {}
+    for i in bands:
+        b = lay.bands[i]
+        u = np.zeros((xb.shape[0], b.M), dtype=np.complex128)
+        u[:, b.slots] = b.g * X[:, b.k_lo:b.k_hi + 1]
+        out[i] = band_idft(u, mode).reshape(*lead, b.M)
+    return out
+
+
 def _half_to_real(lay: Layout, Y: np.ndarray) -> np.ndarray:
     """Real signal whose spectrum is Y on 0..N/2 extended by conjugate symmetry."""
     N, half = lay.N, lay.half

@@ -13,7 +13,6 @@
 
 namespace nsg {
 
-constexpr int kWrSlots = 64;   // LDS complex slots reserved for a generic radix table
 static_assert(kGenericMaxRadix <= kWrSlots, "generic radix table exceeds its LDS slots");
 
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
@@ -33,6 +32,8 @@ struct Tables {
     const float2* tw4_lo;
     const float* slicewin;
     const WorkItem* items;   // work items of the band kernels, all buckets
+    const BigDesc* bigs;     // huge bands
+    const BigItem* bigitems; // work items of the huge-band passes
 };
 
 struct Pass {
@@ -366,6 +367,151 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
         float2 u = buf[lp(__mul24(sg, n) + slot)];
         if (blu) u = cmul(ch[slot], conjf2(u));
         W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, w[i]);
+    }
+}
+
+// ------------------------------------------------------------ huge bands
+// Bands whose transform exceeds one workgroup run the same router, band DFTs
+// and weighting as k_band_analysis / k_band_synthesis, but transform through
+// a four-step FFT n = n1 n2 in a per-signal global buffer: the column pass
+// (k_big_a) builds its input on the fly, the row pass (k_big_b) finishes the
+// output.
+
+struct BigArgs {
+    const float2* Z;        // analysis input, [b][L]
+    const float2* cin;      // synthesis input, [b][C]
+    float2* cout;           // analysis output, [b][C]
+    float2* W;              // synthesis output (weighted band spectra), [b][C]
+    float2* H1;             // four-step intermediate, [b][Hn]
+    float2* H2;             // Bluestein first-FFT output, [b][Hn]
+    const float* wt;        // per-coefficient weights of the op
+    int L;
+    long long C, Hn;
+    int analysis;
+};
+
+constexpr int kBigInRoute = 0, kBigInCoef = 1, kBigInBlu2 = 2;
+
+__device__ __forceinline__ void big_lds(float2* lds, const FftDesc* fdn, float2*& wr, float2*& twl, float2*& t4,
+                                        float2*& buf) {
+    wr = lds;
+    twl = lds + kWrSlots;
+    t4 = twl + kTwSlots;
+    buf = t4 + fdn->nhi + (1 << fdn->lg);
+}
+
+// Column pass: input element j of the length-n sequence, columns c0..c0+cols
+// of the n1 x n2 view j = r n2 + c, length-n1 DFTs, twiddle omega_n^{c k1}.
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int item0, int nitems, int batch,
+                                                      int in_mode) {
+    extern __shared__ float2 lds[];
+    const BigItem it = T.bigitems[item0 + xcd_remap(blockIdx.x, nitems)];
+    if (it.sig >= batch) return;
+    const BigDesc bg = T.bigs[it.big];
+    const BandDev bd = T.bands[bg.band];
+    const FftDesc* fdn = T.ffts + bg.fftn;
+    float2 *wr, *twl, *t4, *buf;
+    big_lds(lds, fdn, wr, twl, t4, buf);
+    const int nt4 = fdn->nhi + (1 << fdn->lg);
+    for (int i = threadIdx.x; i < nt4; i += NT) t4[i] = T.tw[fdn->tw + fdn->n + i];
+    const TwL w4{t4, fdn->nhi, fdn->lg};
+    const int M = bd.M;
+    const bool blu = bd.chirp >= 0;
+    const int c0 = it.tile * bg.tile_a;
+    const int cols = min(bg.tile_a, bg.n2 - c0);
+    const int tot = cols * bg.n1;
+    const Div dc = mkdiv(cols);
+    const long long hbase = (long long)it.sig * a.Hn + bg.hoff;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        int c;
+        const int r = qdiv(e, dc, c);
+        const int j = __mul24(r, bg.n2) + c0 + c;
+        float2 v = make_float2(0.f, 0.f);
+        if (in_mode == kBigInBlu2) {
+            v = conjf2(cmul(a.H2[hbase + j], T.kern[bd.kern + j]));
+        } else if (j < M) {
+            if (in_mode == kBigInRoute) {
+                int i = j - bd.rot;
+                if (i < 0) i += M;
+                const int k = bd.k_lo + i;
+                const float2* Zs = a.Z + (long long)it.sig * a.L;
+                const int ka = (k == a.L) ? 0 : k;
+                const int kb = (ka == 0) ? 0 : a.L - ka;
+                const float2 za = Zs[ka], zb = Zs[kb];
+                const float2 om = T.omega[k];
+                const float2 pa = make_float2(1.f + om.y, -om.x);
+                const float2 pb = make_float2(1.f - om.y, om.x);
+                const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
+                const float hw = 0.5f * a.wt[bd.off + i];
+                v = make_float2(hw * u2.x, -hw * u2.y);          // conj(u)
+            } else {
+                v = a.cin[(long long)it.sig * a.C + bd.off + j];
+            }
+            if (blu) v = cmul(v, T.chirp[bd.chirp + j]);
+        }
+        buf[lp(__mul24(c, bg.ld_a) + r)] = v;
+    }
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, cols, bg.ld_a, T.ffts + bg.fft1, T.tw, wr, twl);
+    __syncthreads();
+    float2* Y = a.H1 + hbase;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        int c;
+        const int k1 = qdiv(e, dc, c);
+        Y[__mul24(k1, bg.n2) + c0 + c] = cmul(buf[lp(__mul24(c, bg.ld_a) + k1)], tw_at(w4, __mul24(c0 + c, k1)));
+    }
+}
+
+// Row pass: rows r0..r0+rows of the intermediate, length-n2 DFTs, output
+// k = k1 + n1 k2. second == 0: a Bluestein band's first FFT goes to H2, any
+// other band finishes; second == 1: the Bluestein band finishes.
+template <int NT, int EPT>
+__global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int item0, int nitems, int batch,
+                                                      int second) {
+    extern __shared__ float2 lds[];
+    const BigItem it = T.bigitems[item0 + xcd_remap(blockIdx.x, nitems)];
+    if (it.sig >= batch) return;
+    const BigDesc bg = T.bigs[it.big];
+    const BandDev bd = T.bands[bg.band];
+    float2* wr = lds;
+    float2* twl = lds + kWrSlots;
+    float2* buf = twl + kTwSlots;
+    const int M = bd.M;
+    const bool blu = bd.chirp >= 0;
+    const int r0 = it.tile * bg.tile_b;
+    const int rows = min(bg.tile_b, bg.n1 - r0);
+    const int tot = rows * bg.n2;
+    const Div dn2 = mkdiv(bg.n2), drows = mkdiv(rows);
+    const long long hbase = (long long)it.sig * a.Hn + bg.hoff;
+    const float2* Y = a.H1 + hbase + (long long)r0 * bg.n2;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        int c;
+        const int r = qdiv(e, dn2, c);
+        buf[lp(__mul24(r, bg.ld_b) + c)] = Y[e];
+    }
+    __syncthreads();
+    lds_fft<NT, EPT>(buf, rows, bg.ld_b, T.ffts + bg.fft2, T.tw, wr, twl);
+    const bool to_mid = blu && !second;
+    for (int e = threadIdx.x; e < tot; e += NT) {
+        int r;
+        const int k2 = qdiv(e, drows, r);
+        const int k = r0 + r + __mul24(bg.n1, k2);
+        const float2 v = buf[lp(__mul24(r, bg.ld_b) + k2)];
+        if (to_mid) {
+            a.H2[hbase + k] = v;
+        } else if (k < M) {
+            if (a.analysis) {
+                // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch) D / M
+                const float2 o = blu ? cmul(conjf2(T.chirp[bd.chirp + k]), v) : conjf2(v);
+                a.cout[(long long)it.sig * a.C + bd.off + k] = cscale(o, bd.inv_M);
+            } else {
+                const float2 u = blu ? cmul(T.chirp[bd.chirp + k], conjf2(v)) : v;
+                int i = k - bd.rot;
+                if (i < 0) i += M;
+                a.W[(long long)it.sig * a.C + bd.off + i] = cscale(u, a.wt[bd.off + i]);
+            }
+        }
     }
 }
 

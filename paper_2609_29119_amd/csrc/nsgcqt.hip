@@ -73,6 +73,8 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iLo = add(h.tw4_lo.data(), h.tw4_lo.size() * sizeof(float));
     const size_t iWin = add(h.slicewin.data(), h.slicewin.size() * sizeof(float));
     const size_t iItems = add(h.items.data(), h.items.size() * sizeof(WorkItem));
+    const size_t iBigs = add(h.bigs.data(), h.bigs.size() * sizeof(BigDesc));
+    const size_t iBigItems = add(h.bigitems.data(), h.bigitems.size() * sizeof(BigItem));
     const size_t iWA = add(h.wA.data(), h.wA.size() * sizeof(float));
     const size_t iWS = add(h.wS.data(), h.wS.size() * sizeof(float));
     const size_t iWT = add(h.wT.data(), h.wT.size() * sizeof(float));
@@ -99,6 +101,8 @@ int upload(nsgcqt_plan_s* p) {
     T.tw4_lo = static_cast<const float2*>(at(iLo));
     T.slicewin = static_cast<const float*>(at(iWin));
     T.items = static_cast<const WorkItem*>(at(iItems));
+    T.bigs = static_cast<const BigDesc*>(at(iBigs));
+    T.bigitems = static_cast<const BigItem*>(at(iBigItems));
     p->wA = static_cast<const float*>(at(iWA));
     p->wS = static_cast<const float*>(at(iWS));
     p->wT = static_cast<const float*>(at(iWT));
@@ -229,6 +233,43 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
     return NSGCQT_OK;
 }
 
+// Huge bands: column pass and row pass over every huge band, then for the
+// Bluestein ones the second FFT (column pass reading H2, row pass finishing).
+int run_big(nsgcqt_plan_s* p, BigArgs a, int batch, hipStream_t s) {
+    const HostPlan& h = p->h;
+    if (h.bigs.empty()) return NSGCQT_OK;
+    auto ka = k_big_a<512, 8>;
+    auto kb = k_big_b<512, 8>;
+    if (int r = launch_prep(ka, h.big_lds_a)) return r;
+    if (int r = launch_prep(kb, h.big_lds_b)) return r;
+    const int in0 = a.analysis ? kBigInRoute : kBigInCoef;
+    for (int pass = 0; pass < 4; ++pass) {
+        const int n = h.big_n[pass];
+        if (n == 0) continue;
+        if (pass % 2 == 0)
+            hipLaunchKernelGGL(ka, dim3(n), dim3(512), h.big_lds_a, s, a, p->T, h.big_off[pass], n, batch,
+                               pass == 0 ? in0 : kBigInBlu2);
+        else
+            hipLaunchKernelGGL(kb, dim3(n), dim3(512), h.big_lds_b, s, a, p->T, h.big_off[pass], n, batch,
+                               pass == 3 ? 1 : 0);
+        HIP_TRY(hipGetLastError());
+        record(p, s);
+    }
+    return NSGCQT_OK;
+}
+
+BigArgs big_args(nsgcqt_plan_s* p, char* ws, int64_t hoff, int batch, bool analysis) {
+    const HostPlan& h = p->h;
+    BigArgs a{};
+    a.H1 = reinterpret_cast<float2*>(ws + hoff);
+    a.H2 = reinterpret_cast<float2*>(ws + hoff + align256(8 * h.Hn * batch));
+    a.L = static_cast<int>(h.L);
+    a.C = h.C;
+    a.Hn = h.Hn;
+    a.analysis = analysis ? 1 : 0;
+    return a;
+}
+
 // Analysis chain (T, or S^dagger with its weights) for `batch` signals or slices.
 int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float* wt, int batch, SliceIn sl,
                   char* ws, hipStream_t s) {
@@ -237,7 +278,12 @@ int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float*
     float2* Z = reinterpret_cast<float2*>(ws + align256(8 * h.L * batch));
     if (int r = run_fwd_a(p, x, Y, batch, sl, static_cast<long long>(h.N), s)) return r;
     if (int r = run_pass_b<false>(p, Y, Z, batch, static_cast<long long>(h.L), s)) return r;
-    return run_bands(p, true, Z, coeffs, wt, batch, s);
+    if (int r = run_bands(p, true, Z, coeffs, wt, batch, s)) return r;
+    BigArgs a = big_args(p, ws, h.off_h_an, h.spc ? h.spc : batch, true);
+    a.Z = Z;
+    a.cout = coeffs;
+    a.wt = wt;
+    return run_big(p, a, batch, s);
 }
 
 // Synthesis chain (S, or T^dagger with its weights); output is [batch][N] f32.
@@ -247,6 +293,11 @@ int chain_synthesise(nsgcqt_plan_s* p, const float2* coeffs, float* xo, const fl
     float2* W = reinterpret_cast<float2*>(ws);
     float2* Y = reinterpret_cast<float2*>(ws + align256(8 * h.C * batch));
     if (int r = run_bands(p, false, coeffs, W, wt, batch, s)) return r;
+    BigArgs a = big_args(p, ws, h.off_h_syn, h.spc ? h.spc : batch, false);
+    a.cin = coeffs;
+    a.W = W;
+    a.wt = wt;
+    if (int r = run_big(p, a, batch, s)) return r;
     if (int r = run_inv_a(p, W, Y, batch, s)) return r;
     return run_pass_b<true>(p, Y, reinterpret_cast<float2*>(xo), batch, static_cast<long long>(h.L), s);
 }
@@ -450,7 +501,7 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, floa
     const int64_t J = nsgcqt_sliced_count(p, n);
     const int64_t H = h.N / 2;
     char* w = static_cast<char*>(ws);
-    const int64_t chain_bytes = align256(8 * h.C * h.spc) + align256(8 * h.L * h.spc);
+    const int64_t chain_bytes = h.off_y_sliced;
     float* y = reinterpret_cast<float*>(w + chain_bytes);
     float* carry[2] = {reinterpret_cast<float*>(w + chain_bytes + align256(4 * h.N * h.spc)),
                        reinterpret_cast<float*>(w + chain_bytes + align256(4 * h.N * h.spc) + align256(4 * H))};
@@ -499,10 +550,29 @@ int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, doub
             st.push_back({"band_analysis_" + std::to_string(bk.nt) + "x" + std::to_string(bk.ept),
                           (cb / C * 8.0 * L + 8.0 * cb) * b});
         }
+    }
+    // huge-band passes: the column pass reads its input share and writes the
+    // intermediate, the row pass reads it and writes the output or the
+    // Bluestein midpoint
+    const double hn = static_cast<double>(h.Hn), hb = static_cast<double>(h.Hn_blu), cg = static_cast<double>(h.C_big);
+    std::vector<St> big;
+    if (!h.bigs.empty()) {
+        const double in0 = an ? cg / C * 8.0 * L : 8.0 * cg;
+        big.push_back({an ? "big_analysis_a" : "big_synthesis_a", (in0 + 8.0 * hn) * b});
+        const double cbb = static_cast<double>(h.C_big_blu);
+        big.push_back({an ? "big_analysis_b" : "big_synthesis_b", (8.0 * hn + 8.0 * (cg - cbb) + 8.0 * hb) * b});
+        if (h.big_n[2]) {
+            big.push_back({an ? "big_analysis_a2" : "big_synthesis_a2", 16.0 * hb * b});
+            big.push_back({an ? "big_analysis_b2" : "big_synthesis_b2", (8.0 * hb + 8.0 * cbb) * b});
+        }
+    }
+    if (an) {
+        st.insert(st.end(), big.begin(), big.end());
     } else {
         for (const auto& bk : h.buckets)
             st.push_back({"band_synthesis_" + std::to_string(bk.nt) + "x" + std::to_string(bk.ept),
                           16.0 * static_cast<double>(bk.coeffs) * b});
+        st.insert(st.end(), big.begin(), big.end());
         st.push_back({"fft_inv_a_overlap_add", (8.0 * C + 8.0 * L) * b});
         st.push_back({"fft_inv_b", 16.0 * L * b});
     }

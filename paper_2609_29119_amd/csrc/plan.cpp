@@ -124,7 +124,6 @@ struct FftRegistry {
         d.nhi = static_cast<int32_t>((n + (int64_t(1) << lg) - 1) >> lg);
         for (int64_t i = 0; i < d.nhi; ++i) push_c(p.twpool, root(i << lg, n));
         for (int64_t j = 0; j < (int64_t(1) << lg); ++j) push_c(p.twpool, root(j, n));
-        if (d.nhi + (1 << lg) > kTwSlots) return -1;
         p.ffts.push_back(d);
         const int id = static_cast<int>(p.ffts.size()) - 1;
         index[n] = id;
@@ -379,15 +378,49 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         bk.nt = t.nt; bk.ept = t.ept; bk.max_work = 0; bk.coeffs = 0;
         p.buckets.push_back(bk);
     }
+    p.bigs.clear(); p.bigitems.clear(); p.Hn = 0; p.C_big = 0; p.Hn_blu = 0; p.C_big_blu = 0;
+    int big_t4 = 0, big_ea = 0, big_eb = 0;
     for (size_t l = 0; l < p.bands.size(); ++l) {
         int ti = -1;
         for (int i = 0; i < 5; ++i)
             if (work[l] <= tiers[i].max_work) { ti = i; break; }
-        if (ti < 0)
-            return fail(err, NSGCQT_EUNSUPPORTED,
-                        "band of length " + std::to_string(p.bands[l].M) +
-                            " needs a transform of " + std::to_string(work[l]) +
-                            " points, above the 16384 one workgroup holds");
+        if (ti < 0) {
+            // four-step through global memory: n = n1 n2, n1 <= n2 <= 4096
+            const int64_t n = work[l];
+            int64_t n1 = -1;
+            for (int64_t d = 2; d * d <= n; ++d) {
+                std::vector<int> r1, r2;
+                if (n % d == 0 && n / d <= 4096 && factor_radices(d, r1) && factor_radices(n / d, r2)) n1 = d;
+            }
+            if (n1 < 0)
+                return fail(err, NSGCQT_EUNSUPPORTED,
+                            "band of length " + std::to_string(p.bands[l].M) + " needs a transform of " +
+                                std::to_string(n) + " points with no supported four-step split");
+            BigDesc g{};
+            g.band = static_cast<int32_t>(l);
+            g.n = static_cast<int32_t>(n);
+            g.n1 = static_cast<int32_t>(n1);
+            g.n2 = static_cast<int32_t>(n / n1);
+            g.fftn = reg.get(n);
+            g.fft1 = reg.get(g.n1);
+            g.fft2 = reg.get(g.n2);
+            if (g.fftn < 0 || g.fft1 < 0 || g.fft2 < 0)
+                return fail(err, NSGCQT_EUNSUPPORTED, "huge band transform has no radix plan");
+            g.tile_a = std::max(1, std::min<int>(16, std::min<int>(4096 / g.n1, g.n2)));
+            g.tile_b = std::max(1, std::min<int>(16, std::min<int>(4096 / g.n2, g.n1)));
+            g.ld_a = g.n1 | 1;
+            g.ld_b = g.n2 | 1;
+            g.hoff = static_cast<int32_t>(p.Hn);
+            p.Hn += n;
+            p.C_big += p.bands[l].M;
+            if (p.banddev[l].chirp >= 0) { p.Hn_blu += n; p.C_big_blu += p.bands[l].M; }
+            const FftDesc& fn = p.ffts[g.fftn];
+            big_t4 = std::max(big_t4, fn.nhi + (1 << fn.lg));
+            big_ea = std::max(big_ea, g.tile_a * g.ld_a);
+            big_eb = std::max(big_eb, g.tile_b * g.ld_b);
+            p.bigs.push_back(g);
+            continue;
+        }
         auto& bk = p.buckets[ti];
         bk.bands.push_back(static_cast<int32_t>(l));
         bk.max_work = std::max(bk.max_work, work[l]);
@@ -413,6 +446,24 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         bk.nitems = static_cast<int>(p.items.size()) - bk.item_off;
     }
 
+    // huge-band work items: pass 0/1 over every huge band, pass 2/3 over the
+    // Bluestein ones (their second FFT)
+    for (int pass = 0; pass < 4; ++pass) {
+        p.big_off[pass] = static_cast<int>(p.bigitems.size());
+        for (size_t gi = 0; gi < p.bigs.size(); ++gi) {
+            const BigDesc& g = p.bigs[gi];
+            if (pass >= 2 && p.banddev[g.band].chirp < 0) continue;
+            const int tiles = (pass % 2 == 0) ? (g.n2 + g.tile_a - 1) / g.tile_a : (g.n1 + g.tile_b - 1) / g.tile_b;
+            for (int sg = 0; sg < batch; ++sg)
+                for (int t = 0; t < tiles; ++t) p.bigitems.push_back(BigItem{static_cast<int32_t>(gi), sg, t, 0});
+        }
+        p.big_n[pass] = static_cast<int>(p.bigitems.size()) - p.big_off[pass];
+    }
+    p.big_lds_a = static_cast<int>((kWrSlots + kTwSlots + big_t4 + lds_slots(big_ea)) * 8);
+    p.big_lds_b = static_cast<int>((kWrSlots + kTwSlots + lds_slots(big_eb)) * 8);
+    if (!p.bigs.empty() && (p.big_lds_a > 160 * 1024 || p.big_lds_b > 160 * 1024))
+        return fail(err, NSGCQT_EUNSUPPORTED, "huge-band pass exceeds LDS");
+
     // ---- slicing window (Sec. 4): zero, sin^2 rise, flat, cos^2 fall, zero
     p.slicewin.clear();
     if (sliced) {
@@ -429,8 +480,12 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
 
     // ---- workspace
     const int64_t b = batch;
-    p.ws_an = 2 * align256(8 * L * b);
-    p.ws_syn = align256(8 * p.C * b) + align256(8 * L * b);
+    const int64_t hbytes = p.Hn ? 2 * align256(8 * p.Hn * b) : 0;
+    p.off_h_an = 2 * align256(8 * L * b);
+    p.ws_an = p.off_h_an + hbytes;
+    p.off_h_syn = align256(8 * p.C * b) + align256(8 * L * b);
+    p.off_y_sliced = p.off_h_syn + hbytes;
+    p.ws_syn = p.off_y_sliced;
     if (sliced) p.ws_syn += align256(4 * N * b) + 2 * align256(4 * (N / 2));
     return NSGCQT_OK;
 }

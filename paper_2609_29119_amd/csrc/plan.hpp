@@ -70,9 +70,21 @@ struct HostPlan {
     std::vector<float> slicewin;            // sliced plans: window of length N
     std::vector<Bucket> buckets;
     std::vector<WorkItem> items;
+
+    // huge bands (transform above one workgroup): descriptors, work items of
+    // the four passes (all bands: column, row; Bluestein only: column, row)
+    std::vector<BigDesc> bigs;
+    std::vector<BigItem> bigitems;
+    int big_off[4] = {0, 0, 0, 0}, big_n[4] = {0, 0, 0, 0};
+    int64_t Hn = 0;             // complex values per signal in each huge-band buffer
+    int64_t C_big = 0;          // coefficients of huge bands
+    int64_t Hn_blu = 0;         // part of Hn that belongs to Bluestein bands
+    int64_t C_big_blu = 0;      // coefficients of huge Bluestein bands
+    int big_lds_a = 0, big_lds_b = 0;   // LDS bytes of the column / row passes
     FourStep fs4{};
 
     int64_t ws_an = 0, ws_syn = 0;
+    int64_t off_h_an = 0, off_h_syn = 0, off_y_sliced = 0;   // workspace offsets
 };
 
 // Returns 0 on success, or a negative nsgcqt status with `err` set.

@@ -29,6 +29,8 @@ struct FftDesc {
 
 // LDS slots reserved for the two-level twiddles of any length up to 16384.
 constexpr int kTwSlots = 288;
+// LDS slots reserved for the table of a generic odd-prime radix.
+constexpr int kWrSlots = 64;
 
 // One band of the layout as the band kernels see it.
 struct BandDev {
@@ -47,6 +49,27 @@ struct WorkItem {
     int32_t band;
     int32_t s0;
     int32_t count;
+    int32_t pad;
+};
+
+// A band whose transform (length M, or Bluestein P) exceeds one workgroup's
+// LDS: it is transformed by a four-step FFT n = n1 * n2 through a per-signal
+// global buffer (region hoff .. hoff + n of each signal's huge-band buffer).
+struct BigDesc {
+    int32_t band;
+    int32_t n, n1, n2;
+    int32_t fftn;            // FftDesc of n: its tables give omega_n for the four-step twiddles
+    int32_t fft1, fft2;      // FftDescs of the column (n1) and row (n2) transforms
+    int32_t tile_a, tile_b;  // columns / rows per workgroup
+    int32_t ld_a, ld_b;
+    int32_t hoff;
+};
+
+// One workgroup of a huge-band pass: band big, signal sig, tile index tile.
+struct BigItem {
+    int32_t big;
+    int32_t sig;
+    int32_t tile;
     int32_t pad;
 };
 

@@ -186,6 +186,50 @@ def test_sliced_long_full_length():
         assert oracle.rel_l2(cg[s], ref) <= REL_TOL
 
 
+def test_long_full_length():
+    # 1 x 2,880,000 at 48 kHz, 96 bins/oct: 984 bands, 116 of them above one
+    # workgroup (four-step through global memory, Bluestein up to P = 42,000).
+    w = workloads.WORKLOADS["long"]
+    lay = oracle.build_layout(*w.plan_args)
+    p = nb.Plan(*w.plan_args, batch=1)
+    x = workloads.signals(w)
+    c = p.analyse(to_gpu(x))
+    xr = to_np(p.synthesise(c))
+    assert oracle.snr_db(x, xr).min() >= SNR_MIN
+    cg = to_np(c)[0]
+    Ms = np.array([b.M for b in lay.bands])
+    big = list(np.argsort(Ms)[-6:])                       # the largest bands
+    rng = np.random.default_rng(0)
+    pick = sorted(set(big) | set(rng.choice(len(lay.bands), 10, replace=False).tolist()) | {0, len(lay.bands) - 1})
+    ref = oracle.analyse_bands(lay, x[0], pick)
+    got = np.concatenate([cg[lay.bands[i].offset:lay.bands[i].offset + lay.bands[i].M] for i in pick])
+    want = np.concatenate([ref[i] for i in pick])
+    assert oracle.rel_l2(got, want) <= REL_TOL
+    # adjoints against the oracle's library-FFT mode (pinned against the direct DFT)
+    y = workloads.coeff_cotangent(w.cot_seed, 1, p.n_coeffs)
+    ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
+    assert oracle.rel_l2(ta, oracle.adjoint_analysis(lay, y, mode="fft")).max() <= REL_TOL
+    xs = workloads.signal_cotangent(w.cot_seed, 1, w.n_samples)
+    sa = to_np(p.adjoint(nb.OP_ADJ_SYNTHESIS, to_gpu(xs)))
+    assert oracle.rel_l2(sa, oracle.adjoint_synthesis(lay, xs, mode="fft")).max() <= REL_TOL
+
+
+def test_huge_bands_small_layout():
+    # a small signal whose top bands exceed one workgroup: N = 2 * 40,000 at
+    # 8 bins per octave puts bands of ~18,000 bins above 16,384 points
+    fs, fmin, fmax, B, N = 80000.0, 2000.0, 40000.0, 2, 80000
+    lay = oracle.build_layout(fs, fmin, fmax, B, N)
+    p = nb.Plan(fs, fmin, fmax, B, N, 2)
+    x = workloads.white(77, 2, N)
+    c = p.analyse(to_gpu(x))
+    cg = to_np(c)
+    assert oracle.rel_l2(cg, oracle.analyse(lay, x, mode="fft")).max() <= REL_TOL
+    assert oracle.snr_db(x, to_np(p.synthesise(c))).min() >= SNR_MIN
+    y = workloads.coeff_cotangent(78, 2, p.n_coeffs)
+    ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
+    assert oracle.rel_l2(ta, oracle.adjoint_analysis(lay, y, mode="fft")).max() <= REL_TOL
+
+
 def test_workspace_too_small_raises():
     w = workloads.WORKLOADS["tiny"]
     p = nb.Plan(*w.plan_args, batch=1)

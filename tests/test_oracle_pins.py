@@ -264,6 +264,15 @@ def test_synthesis_adjoint_by_sums():
     np.testing.assert_allclose(oracle.adjoint_synthesis(lay, x), ref, atol=1e-12)
 
 
+def test_band_subset_matches_full_analysis():
+    lay = small_layout(N=250, fs=250.0, fmin=4.0, fmax=125.0, B=4)
+    x = np.random.default_rng(4).standard_normal((2, lay.N))
+    full = oracle.split_bands(lay, oracle.analyse(lay, x))
+    sub = oracle.analyse_bands(lay, x, [0, 3, len(lay.bands) - 1])
+    for i, v in sub.items():
+        np.testing.assert_allclose(v, full[i], atol=1e-13)
+
+
 def test_direct_and_fft_modes_agree():
     lay = small_layout(N=250, fs=250.0, fmin=4.0, fmax=125.0, B=4)
     x = np.random.default_rng(2).standard_normal(lay.N)
