@@ -38,6 +38,8 @@ def build(verbose: bool = False) -> str:
     """Compile every source and link the shared library; returns its path."""
     hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     os.makedirs(BUILD, exist_ok=True)
+    _run([sys.executable, os.path.join(CSRC, "gen_radix_consts.py"), os.path.join(CSRC, "radix_consts.hpp")],
+         verbose)
     plan_o = os.path.join(BUILD, "plan.o")
     hip_o = os.path.join(BUILD, "nsgcqt.o")
     _run(["g++", "-O2", "-std=c++17", "-fPIC", "-Wall", "-c",

@@ -5,6 +5,10 @@
 //   Y      L complex64, row k1 of length L2  four-step intermediate
 //   Z      L complex64, natural order         packed spectrum Z = F_L P x
 //   c / W  C complex64, band offsets          coefficients / weighted band spectra
+//
+// Every kernel stages its sequences in LDS as 2^lgnb interleaved sequences
+// (element i of sequence t at i*S + t, see fft_lds.hpp) and transforms them
+// with lds_fft.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -38,10 +42,10 @@ struct Tables {
 
 struct Pass {
     int L1, L2;
-    int tile;                // columns (pass A) or rows (pass B) per workgroup
+    int lgnb;                // log2 of the columns (pass A) or rows (pass B) per workgroup
     int ntile;
-    int ld;
     int fft;                 // FftDesc index of the pass length
+    int ntw;                 // its stage-twiddle count
     int split;               // four-step twiddles: hi[t >> split] * lo[t & (2^split - 1)]
     int nhi4;                // number of hi values
     int L;
@@ -63,14 +67,14 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
     return x * q + (x < r ? x : r) + i;
 }
 
-// LDS layout of the pass kernels: generic radix table, FFT twiddles, the
-// four-step twiddles (hi then lo) and the data.
-__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, float2*& wr, float2*& twl, float2*& t4,
-                                         float2*& buf) {
+// LDS of the pass kernels: generic radix table, stage twiddles, four-step
+// twiddles (hi then lo, pass A only), data.
+__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_tw4, float2*& wr, float2*& tws,
+                                         float2*& t4, float2*& buf) {
     wr = lds;
-    twl = lds + kWrSlots;
-    t4 = twl + kTwSlots;
-    buf = t4 + p.nhi4 + (1 << p.split);
+    tws = wr + kWrSlots;
+    t4 = tws + p.ntw;
+    buf = t4 + (with_tw4 ? p.nhi4 + (1 << p.split) : 0);
 }
 
 template <int NT>
@@ -91,46 +95,49 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
                                                       Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
     extern __shared__ float2 lds[];
-    float2 *wr, *twl, *t4, *buf;
-    pass_lds(lds, p, wr, twl, t4, buf);
+    float2 *wr, *tws, *t4, *buf;
+    pass_lds(lds, p, true, wr, tws, t4, buf);
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
-    const int n2a = tile * p.tile;
-    const int cols = min(p.tile, p.L2 - n2a);
-    const int tot = cols * p.L1;
-    const Div dc = mkdiv(cols);
+    const int nbm = (1 << p.lgnb) - 1, S = seq_stride(p.lgnb);
+    const int n2a = tile << p.lgnb;
+    const int cols = min(nbm + 1, p.L2 - n2a);
+    const int tot = p.L1 << p.lgnb;
     if (!sl.enabled) {
         const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
         for (int e = threadIdx.x; e < tot; e += NT) {
-            int c;
-            const int n1 = qdiv(e, dc, c);
-            buf[lp(__mul24(c, p.ld) + n1)] = z[__mul24(n1, p.L2) + n2a + c];
+            const int c = e & nbm, n1 = e >> p.lgnb;
+            buf[__mul24(n1, S) + c] = c < cols ? z[__mul24(n1, p.L2) + n2a + c] : make_float2(0.f, 0.f);
         }
     } else {
         // padded coordinate of sample 2j of slice s is s H + 2j; the signal
         // starts at padded H
         const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
         for (int e = threadIdx.x; e < tot; e += NT) {
-            int c;
-            const int n1 = qdiv(e, dc, c);
-            const long long j = (long long)n1 * p.L2 + n2a + c;
-            const long long t = base + 2 * j;
-            const float v0 = (t >= 0 && t < sl.n) ? x[t] : 0.f;
-            const float v1 = (t + 1 >= 0 && t + 1 < sl.n) ? x[t + 1] : 0.f;
-            buf[lp(__mul24(c, p.ld) + n1)] = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
+            const int c = e & nbm, n1 = e >> p.lgnb;
+            float2 v = make_float2(0.f, 0.f);
+            if (c < cols) {
+                const int j = __mul24(n1, p.L2) + n2a + c;
+                const long long t = base + 2 * (long long)j;
+                const float v0 = (t >= 0 && t < sl.n) ? x[t] : 0.f;
+                const float v1 = (t + 1 >= 0 && t + 1 < sl.n) ? x[t + 1] : 0.f;
+                v = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
+            }
+            buf[__mul24(n1, S) + c] = v;
         }
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr, tws);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int c;
-        const int k1 = qdiv(e, dc, c);
-        const int n2 = n2a + c;
-        Ys[__mul24(k1, p.L2) + n2] = cmul(buf[lp(__mul24(c, p.ld) + k1)], tw4(t4, p, __mul24(n2, k1)));
+        const int c = e & nbm, k1 = e >> p.lgnb;
+        if (c < cols) {
+            const int n2 = n2a + c;
+            Ys[__mul24(k1, p.L2) + n2] = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
+        }
     }
 }
 
@@ -153,39 +160,43 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
                                                       Pass p, Tables T, int batch, long long C) {
     extern __shared__ float2 lds[];
-    float2 *wr, *twl, *t4, *buf;
-    pass_lds(lds, p, wr, twl, t4, buf);
+    float2 *wr, *tws, *t4, *buf;
+    pass_lds(lds, p, true, wr, tws, t4, buf);
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
-    const int n2a = tile * p.tile;
-    const int cols = min(p.tile, p.L2 - n2a);
-    const int tot = cols * p.L1;
-    const Div dc = mkdiv(cols);
+    const int nbm = (1 << p.lgnb) - 1, S = seq_stride(p.lgnb);
+    const int n2a = tile << p.lgnb;
+    const int cols = min(nbm + 1, p.L2 - n2a);
+    const int tot = p.L1 << p.lgnb;
     const float2* Ws = W + (long long)sig * C;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int c;
-        const int n1 = qdiv(e, dc, c);
-        const int q = __mul24(n1, p.L2) + n2a + c;
-        float2 xq = gather_bin(T, Ws, q);
-        float2 xm = gather_bin(T, Ws, p.L - q);
-        if (q == 0) { xq.y = 0.f; xm.y = 0.f; }
-        const float2 om = T.omega[q];                         // (cos, -sin)
-        const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w)
-        const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
-        const float2 zq = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
-        buf[lp(__mul24(c, p.ld) + n1)] = make_float2(0.5f * zq.x, -0.5f * zq.y);   // conj(Z_q)
+        const int c = e & nbm, n1 = e >> p.lgnb;
+        float2 v = make_float2(0.f, 0.f);
+        if (c < cols) {
+            const int q = __mul24(n1, p.L2) + n2a + c;
+            float2 xq = gather_bin(T, Ws, q);
+            float2 xm = gather_bin(T, Ws, p.L - q);
+            if (q == 0) { xq.y = 0.f; xm.y = 0.f; }
+            const float2 om = T.omega[q];                         // (cos, -sin)
+            const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w)
+            const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
+            const float2 zq = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
+            v = make_float2(0.5f * zq.x, -0.5f * zq.y);           // conj(Z_q)
+        }
+        buf[__mul24(n1, S) + c] = v;
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, cols, p.ld, T.ffts + p.fft, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr, tws);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int c;
-        const int k1 = qdiv(e, dc, c);
-        const int n2 = n2a + c;
-        Ys[__mul24(k1, p.L2) + n2] = cmul(buf[lp(__mul24(c, p.ld) + k1)], tw4(t4, p, __mul24(n2, k1)));
+        const int c = e & nbm, k1 = e >> p.lgnb;
+        if (c < cols) {
+            const int n2 = n2a + c;
+            Ys[__mul24(k1, p.L2) + n2] = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
+        }
     }
 }
 
@@ -198,37 +209,38 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
                                                        Pass p, Tables T, int batch, long long out_stride,
                                                        float inv_L) {
     extern __shared__ float2 lds[];
-    float2 *wr, *twl, *t4, *buf;
-    pass_lds(lds, p, wr, twl, t4, buf);
-    load_tw4<NT>(t4, p, T);
+    float2 *wr, *tws, *t4, *buf;
+    pass_lds(lds, p, false, wr, tws, t4, buf);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
-    const int k1a = tile * p.tile;
-    const int rows = min(p.tile, p.L1 - k1a);
-    const int tot = rows * p.L2;
-    const Div dl2 = mkdiv(p.L2), drows = mkdiv(rows);
+    const int nbm = (1 << p.lgnb) - 1, S = seq_stride(p.lgnb);
+    const int k1a = tile << p.lgnb;
+    const int rows = min(nbm + 1, p.L1 - k1a);
+    const int tot = p.L2 << p.lgnb;
+    const Div dl2 = mkdiv(p.L2);
     const float2* Ys = Y + (long long)sig * p.L + (long long)k1a * p.L2;
     for (int e = threadIdx.x; e < tot; e += NT) {
         int n2;
         const int r = qdiv(e, dl2, n2);
-        buf[lp(__mul24(r, p.ld) + n2)] = Ys[e];
+        buf[__mul24(n2, S) + r] = r < rows ? Ys[e] : make_float2(0.f, 0.f);
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, rows, p.ld, T.ffts + p.fft, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr, tws);
     float2* os = out + (long long)sig * out_stride;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int r;
-        const int k2 = qdiv(e, drows, r);
-        const int k = k1a + r + __mul24(p.L1, k2);
-        const float2 v = buf[lp(__mul24(r, p.ld) + k2)];
-        os[k] = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
+        const int r = e & nbm, k2 = e >> p.lgnb;
+        if (r < rows) {
+            const float2 v = buf[__mul24(k2, S) + r];
+            os[k1a + r + __mul24(p.L1, k2)] = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
+        }
     }
 }
 
 // ------------------------------------------------------------ band analysis
-// One workgroup per work item (band, signals s0 .. s0 + count - 1). For entry i
-// of the band (bin k = k_lo + i) the router (eq. 7) forms
+// One workgroup per work item (band, signals s0 .. s0 + count - 1, interleaved
+// as 2^lgnb sequences). For entry i of the band (bin k = k_lo + i) the router
+// (eq. 7) forms
 //   u = (1/2) w [(1 - i w_k) Z_{k mod L} + (1 + i w_k) conj(Z_{-k mod L})]
 // with w the band's weight at k (g for T, the S^dagger weight for S^dagger),
 // places conj(u) at slot (k - k_c) mod M in LDS, and the band's inverse DFT
@@ -241,65 +253,61 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
                                                               const float* __restrict__ wt, Tables T, int item0,
                                                               int nitems, int batch, int L, long long C) {
     extern __shared__ float2 lds[];
-    float2* wr = lds;
-    float2* twl = lds + kWrSlots;
-    float2* buf = twl + kTwSlots;
     const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
+    float2* wr = lds;
+    float2* tws = wr + kWrSlots;
+    float2* buf = tws + fd->ntw;
     const int M = bd.M, n = fd->n;
+    const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
     const float* w = wt + bd.off;
     const Div dM = mkdiv(M);
-    for (int e = threadIdx.x; e < g * M; e += NT) {
+    for (int e = threadIdx.x; e < (M << lg); e += NT) {
         int i;
         const int sg = qdiv(e, dM, i);
-        const float2* Zs = Z + (long long)(it.s0 + sg) * L;
-        const int k = bd.k_lo + i;
-        const int a = (k == L) ? 0 : k;
-        const int bm = (a == 0) ? 0 : L - a;
-        const float2 za = Zs[a], zb = Zs[bm];
-        const float2 om = T.omega[k];                         // (cos, -sin)
-        const float2 pa = make_float2(1.f + om.y, -om.x);     // 1 - i w_k
-        const float2 pb = make_float2(1.f - om.y, om.x);      // 1 + i w_k
-        const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
-        const float hw = 0.5f * w[i];
-        float2 v = make_float2(hw * u2.x, -hw * u2.y);        // conj(u)
         int slot = i + bd.rot;
         if (slot >= M) slot -= M;
-        if (blu) v = cmul(v, T.chirp[bd.chirp + slot]);
-        buf[lp(__mul24(sg, n) + slot)] = v;
-    }
-    if (blu) {
-        const int pad = n - M;
-        const Div dp = mkdiv(pad);
-        for (int e = threadIdx.x; e < g * pad; e += NT) {
-            int i;
-            const int sg = qdiv(e, dp, i);
-            buf[lp(__mul24(sg, n) + M + i)] = make_float2(0.f, 0.f);
+        float2 v = make_float2(0.f, 0.f);
+        if (sg < g) {
+            const float2* Zs = Z + (long long)(it.s0 + sg) * L;
+            const int k = bd.k_lo + i;
+            const int a = (k == L) ? 0 : k;
+            const int bm = (a == 0) ? 0 : L - a;
+            const float2 za = Zs[a], zb = Zs[bm];
+            const float2 om = T.omega[k];                         // (cos, -sin)
+            const float2 pa = make_float2(1.f + om.y, -om.x);     // 1 - i w_k
+            const float2 pb = make_float2(1.f - om.y, om.x);      // 1 + i w_k
+            const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
+            const float hw = 0.5f * w[i];
+            v = make_float2(hw * u2.x, -hw * u2.y);               // conj(u)
+            if (blu) v = cmul(v, T.chirp[bd.chirp + slot]);
         }
+        buf[__mul24(slot, S) + sg] = v;
     }
+    if (blu)
+        for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
+            buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
     if (blu) {
         const float2* K = T.kern + bd.kern;
-        const Div dn = mkdiv(n);
-        for (int e = threadIdx.x; e < g * n; e += NT) {
-            int i;
-            qdiv(e, dn, i);
-            const int a = lp(e);
+        for (int e = threadIdx.x; e < (n << lg); e += NT) {
+            const int i = e >> lg;
+            const int a = __mul24(i, S) + (e & (nb - 1));
             buf[a] = conjf2(cmul(buf[a], K[i]));
         }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
+        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
     }
     const float2* ch = T.chirp + (blu ? bd.chirp : 0);
-    for (int e = threadIdx.x; e < g * M; e += NT) {
+    for (int e = threadIdx.x; e < __mul24(g, M); e += NT) {
         int i;
         const int sg = qdiv(e, dM, i);
-        const float2 v = buf[lp(__mul24(sg, n) + i)];
+        const float2 v = buf[__mul24(i, S) + sg];
         float2* cs = coef + (long long)(it.s0 + sg) * C + bd.off;
         // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
         cs[i] = blu ? cscale(cmul(conjf2(ch[i]), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
@@ -316,55 +324,51 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
                                                                const float* __restrict__ wt, Tables T, int item0,
                                                                int nitems, int batch, long long C) {
     extern __shared__ float2 lds[];
-    float2* wr = lds;
-    float2* twl = lds + kWrSlots;
-    float2* buf = twl + kTwSlots;
     const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
+    float2* wr = lds;
+    float2* tws = wr + kWrSlots;
+    float2* buf = tws + fd->ntw;
     const int M = bd.M, n = fd->n;
+    const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
     const float2* ch = T.chirp + (blu ? bd.chirp : 0);
     const Div dM = mkdiv(M);
-    for (int e = threadIdx.x; e < g * M; e += NT) {
+    for (int e = threadIdx.x; e < (M << lg); e += NT) {
         int i;
         const int sg = qdiv(e, dM, i);
-        float2 v = coef[(long long)(it.s0 + sg) * C + bd.off + i];
-        if (blu) v = cmul(v, ch[i]);
-        buf[lp(__mul24(sg, n) + i)] = v;
-    }
-    if (blu) {
-        const int pad = n - M;
-        const Div dp = mkdiv(pad);
-        for (int e = threadIdx.x; e < g * pad; e += NT) {
-            int i;
-            const int sg = qdiv(e, dp, i);
-            buf[lp(__mul24(sg, n) + M + i)] = make_float2(0.f, 0.f);
+        float2 v = make_float2(0.f, 0.f);
+        if (sg < g) {
+            v = coef[(long long)(it.s0 + sg) * C + bd.off + i];
+            if (blu) v = cmul(v, ch[i]);
         }
+        buf[__mul24(i, S) + sg] = v;
     }
+    if (blu)
+        for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
+            buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
     if (blu) {
         const float2* K = T.kern + bd.kern;
-        const Div dn = mkdiv(n);
-        for (int e = threadIdx.x; e < g * n; e += NT) {
-            int i;
-            qdiv(e, dn, i);
-            const int a = lp(e);
+        for (int e = threadIdx.x; e < (n << lg); e += NT) {
+            const int i = e >> lg;
+            const int a = __mul24(i, S) + (e & (nb - 1));
             buf[a] = conjf2(cmul(buf[a], K[i]));
         }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, g, n, fd, T.tw, wr, twl);
+        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
     }
     const float* w = wt + bd.off;
-    for (int e = threadIdx.x; e < g * M; e += NT) {
+    for (int e = threadIdx.x; e < __mul24(g, M); e += NT) {
         int i;
         const int sg = qdiv(e, dM, i);
         int slot = i + bd.rot;
         if (slot >= M) slot -= M;
-        float2 u = buf[lp(__mul24(sg, n) + slot)];
+        float2 u = buf[__mul24(slot, S) + sg];
         if (blu) u = cmul(ch[slot], conjf2(u));
         W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, w[i]);
     }
@@ -392,14 +396,6 @@ struct BigArgs {
 
 constexpr int kBigInRoute = 0, kBigInCoef = 1, kBigInBlu2 = 2;
 
-__device__ __forceinline__ void big_lds(float2* lds, const FftDesc* fdn, float2*& wr, float2*& twl, float2*& t4,
-                                        float2*& buf) {
-    wr = lds;
-    twl = lds + kWrSlots;
-    t4 = twl + kTwSlots;
-    buf = t4 + fdn->nhi + (1 << fdn->lg);
-}
-
 // Column pass: input element j of the length-n sequence, columns c0..c0+cols
 // of the n1 x n2 view j = r n2 + c, length-n1 DFTs, twiddle omega_n^{c k1}.
 template <int NT, int EPT>
@@ -411,55 +407,59 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
     const BigDesc bg = T.bigs[it.big];
     const BandDev bd = T.bands[bg.band];
     const FftDesc* fdn = T.ffts + bg.fftn;
-    float2 *wr, *twl, *t4, *buf;
-    big_lds(lds, fdn, wr, twl, t4, buf);
+    const FftDesc* fd1 = T.ffts + bg.fft1;
+    float2* wr = lds;
+    float2* t4 = wr + kWrSlots;
     const int nt4 = fdn->nhi + (1 << fdn->lg);
-    for (int i = threadIdx.x; i < nt4; i += NT) t4[i] = T.tw[fdn->tw + fdn->n + i];
+    float2* tws = t4 + nt4;
+    float2* buf = tws + fd1->ntw;
+    for (int i = threadIdx.x; i < nt4; i += NT) t4[i] = T.tw[fdn->full + fdn->n + i];
     const TwL w4{t4, fdn->nhi, fdn->lg};
     const int M = bd.M;
     const bool blu = bd.chirp >= 0;
-    const int c0 = it.tile * bg.tile_a;
-    const int cols = min(bg.tile_a, bg.n2 - c0);
-    const int tot = cols * bg.n1;
-    const Div dc = mkdiv(cols);
+    const int lg = bg.lga, nbm = (1 << lg) - 1, S = seq_stride(lg);
+    const int c0 = it.tile << lg;
+    const int cols = min(nbm + 1, bg.n2 - c0);
+    const int tot = bg.n1 << lg;
     const long long hbase = (long long)it.sig * a.Hn + bg.hoff;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int c;
-        const int r = qdiv(e, dc, c);
+        const int c = e & nbm, r = e >> lg;
         const int j = __mul24(r, bg.n2) + c0 + c;
         float2 v = make_float2(0.f, 0.f);
-        if (in_mode == kBigInBlu2) {
-            v = conjf2(cmul(a.H2[hbase + j], T.kern[bd.kern + j]));
-        } else if (j < M) {
-            if (in_mode == kBigInRoute) {
-                int i = j - bd.rot;
-                if (i < 0) i += M;
-                const int k = bd.k_lo + i;
-                const float2* Zs = a.Z + (long long)it.sig * a.L;
-                const int ka = (k == a.L) ? 0 : k;
-                const int kb = (ka == 0) ? 0 : a.L - ka;
-                const float2 za = Zs[ka], zb = Zs[kb];
-                const float2 om = T.omega[k];
-                const float2 pa = make_float2(1.f + om.y, -om.x);
-                const float2 pb = make_float2(1.f - om.y, om.x);
-                const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
-                const float hw = 0.5f * a.wt[bd.off + i];
-                v = make_float2(hw * u2.x, -hw * u2.y);          // conj(u)
-            } else {
-                v = a.cin[(long long)it.sig * a.C + bd.off + j];
+        if (c < cols) {
+            if (in_mode == kBigInBlu2) {
+                v = conjf2(cmul(a.H2[hbase + j], T.kern[bd.kern + j]));
+            } else if (j < M) {
+                if (in_mode == kBigInRoute) {
+                    int i = j - bd.rot;
+                    if (i < 0) i += M;
+                    const int k = bd.k_lo + i;
+                    const float2* Zs = a.Z + (long long)it.sig * a.L;
+                    const int ka = (k == a.L) ? 0 : k;
+                    const int kb = (ka == 0) ? 0 : a.L - ka;
+                    const float2 za = Zs[ka], zb = Zs[kb];
+                    const float2 om = T.omega[k];
+                    const float2 pa = make_float2(1.f + om.y, -om.x);
+                    const float2 pb = make_float2(1.f - om.y, om.x);
+                    const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
+                    const float hw = 0.5f * a.wt[bd.off + i];
+                    v = make_float2(hw * u2.x, -hw * u2.y);          // conj(u)
+                } else {
+                    v = a.cin[(long long)it.sig * a.C + bd.off + j];
+                }
+                if (blu) v = cmul(v, T.chirp[bd.chirp + j]);
             }
-            if (blu) v = cmul(v, T.chirp[bd.chirp + j]);
         }
-        buf[lp(__mul24(c, bg.ld_a) + r)] = v;
+        buf[__mul24(r, S) + c] = v;
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, cols, bg.ld_a, T.ffts + bg.fft1, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, lg, fd1, T.tw, wr, tws);
     __syncthreads();
     float2* Y = a.H1 + hbase;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int c;
-        const int k1 = qdiv(e, dc, c);
-        Y[__mul24(k1, bg.n2) + c0 + c] = cmul(buf[lp(__mul24(c, bg.ld_a) + k1)], tw_at(w4, __mul24(c0 + c, k1)));
+        const int c = e & nbm, k1 = e >> lg;
+        if (c < cols)
+            Y[__mul24(k1, bg.n2) + c0 + c] = cmul(buf[__mul24(k1, S) + c], tw_at(w4, __mul24(c0 + c, k1)));
     }
 }
 
@@ -474,30 +474,32 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int i
     if (it.sig >= batch) return;
     const BigDesc bg = T.bigs[it.big];
     const BandDev bd = T.bands[bg.band];
+    const FftDesc* fd2 = T.ffts + bg.fft2;
     float2* wr = lds;
-    float2* twl = lds + kWrSlots;
-    float2* buf = twl + kTwSlots;
+    float2* tws = wr + kWrSlots;
+    float2* buf = tws + fd2->ntw;
     const int M = bd.M;
     const bool blu = bd.chirp >= 0;
-    const int r0 = it.tile * bg.tile_b;
-    const int rows = min(bg.tile_b, bg.n1 - r0);
-    const int tot = rows * bg.n2;
-    const Div dn2 = mkdiv(bg.n2), drows = mkdiv(rows);
+    const int lg = bg.lgb, nbm = (1 << lg) - 1, S = seq_stride(lg);
+    const int r0 = it.tile << lg;
+    const int rows = min(nbm + 1, bg.n1 - r0);
+    const int tot = bg.n2 << lg;
+    const Div dn2 = mkdiv(bg.n2);
     const long long hbase = (long long)it.sig * a.Hn + bg.hoff;
     const float2* Y = a.H1 + hbase + (long long)r0 * bg.n2;
     for (int e = threadIdx.x; e < tot; e += NT) {
         int c;
         const int r = qdiv(e, dn2, c);
-        buf[lp(__mul24(r, bg.ld_b) + c)] = Y[e];
+        buf[__mul24(c, S) + r] = r < rows ? Y[e] : make_float2(0.f, 0.f);
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, rows, bg.ld_b, T.ffts + bg.fft2, T.tw, wr, twl);
+    lds_fft<NT, EPT>(buf, S, lg, fd2, T.tw, wr, tws);
     const bool to_mid = blu && !second;
     for (int e = threadIdx.x; e < tot; e += NT) {
-        int r;
-        const int k2 = qdiv(e, drows, r);
+        const int r = e & nbm, k2 = e >> lg;
+        if (r >= rows) continue;
         const int k = r0 + r + __mul24(bg.n1, k2);
-        const float2 v = buf[lp(__mul24(r, bg.ld_b) + k2)];
+        const float2 v = buf[__mul24(k2, S) + r];
         if (to_mid) {
             a.H2[hbase + k] = v;
         } else if (k < M) {

@@ -127,24 +127,30 @@ void record(nsgcqt_plan_s* p, hipStream_t s) {
 Pass pass_a(const HostPlan& h) {
     Pass q{};
     q.L1 = static_cast<int>(h.fs4.L1); q.L2 = static_cast<int>(h.fs4.L2);
-    q.tile = h.fs4.tile_a;
-    q.ntile = static_cast<int>((h.fs4.L2 + q.tile - 1) / q.tile);
-    q.ld = h.fs4.ld_a; q.fft = h.fs4.fft1;
-    q.split = static_cast<int>(h.fs4.split); q.L = static_cast<int>(h.L);
+    q.lgnb = h.fs4.tile_a;
+    q.ntile = static_cast<int>((h.fs4.L2 + (int64_t(1) << q.lgnb) - 1) >> q.lgnb);
+    q.fft = h.fs4.fft1;
+    q.ntw = h.ffts[q.fft].ntw;
+    q.split = static_cast<int>(h.fs4.split);
     q.nhi4 = static_cast<int>(h.tw4_hi.size() / 2);
+    q.L = static_cast<int>(h.L);
     return q;
 }
 
 Pass pass_b(const HostPlan& h) {
     Pass q = pass_a(h);
-    q.tile = h.fs4.tile_b;
-    q.ntile = static_cast<int>((h.fs4.L1 + q.tile - 1) / q.tile);
-    q.ld = h.fs4.ld_b; q.fft = h.fs4.fft2;
+    q.lgnb = h.fs4.tile_b;
+    q.ntile = static_cast<int>((h.fs4.L1 + (int64_t(1) << q.lgnb) - 1) >> q.lgnb);
+    q.fft = h.fs4.fft2;
+    q.ntw = h.ffts[q.fft].ntw;
     return q;
 }
 
-int lds_pass(const Pass& q) {
-    return (kWrSlots + kTwSlots + q.nhi4 + (1 << q.split) + lds_slots(q.tile * q.ld)) * static_cast<int>(sizeof(float2));
+int lds_pass_a(const Pass& q) {
+    return (kWrSlots + q.ntw + q.nhi4 + (1 << q.split) + lds_slots(q.L1, q.lgnb)) * static_cast<int>(sizeof(float2));
+}
+int lds_pass_b(const Pass& q) {
+    return (kWrSlots + q.ntw + lds_slots(q.L2, q.lgnb)) * static_cast<int>(sizeof(float2));
 }
 
 #define DISPATCH_NT(nt, KERNEL, ...)                                                         \
@@ -157,7 +163,7 @@ int lds_pass(const Pass& q) {
 int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl, long long sig_stride,
               hipStream_t s) {
     const Pass q = pass_a(p->h);
-    const int lds = lds_pass(q);
+    const int lds = lds_pass_a(q);
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
         hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch,
@@ -172,7 +178,7 @@ int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl
 
 int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream_t s) {
     const Pass q = pass_a(p->h);
-    const int lds = lds_pass(q);
+    const int lds = lds_pass_a(q);
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
         hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, W, Y, q, p->T, batch,
@@ -188,7 +194,7 @@ int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream
 template <bool INV>
 int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long long out_stride, hipStream_t s) {
     const Pass q = pass_b(p->h);
-    const int lds = lds_pass(q);
+    const int lds = lds_pass_b(q);
     const float inv_L = static_cast<float>(1.0 / static_cast<double>(p->h.L));
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
@@ -206,7 +212,7 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
               hipStream_t s) {
     const HostPlan& h = p->h;
     for (const auto& bk : h.buckets) {
-        const int lds = (kWrSlots + kTwSlots + lds_slots(bk.lds_elems)) * static_cast<int>(sizeof(float2));
+        const int lds = (kWrSlots + bk.lds_elems) * static_cast<int>(sizeof(float2));
         const dim3 grid(bk.nitems), block(bk.nt);
         auto go = [&](auto ka, auto ks) -> int {
             if (analysis) {

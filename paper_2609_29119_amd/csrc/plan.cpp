@@ -72,24 +72,36 @@ void push_c(std::vector<float>& v, cd z) {
 bool factor_radices(int64_t n, std::vector<int>& out) {
     out.clear();
     if (n < 1) return false;
+    // prime factors, largest first
+    std::vector<int64_t> f;
     int64_t m = n;
-    int e2 = 0;
-    while (m % 2 == 0) { m /= 2; ++e2; }
-    // powers of two as radix-8 stages, with a radix-4 pair or a single 4 or 2
-    // for the remainder
-    if (e2 % 3 == 1 && e2 >= 4) { out.push_back(4); out.push_back(4); e2 -= 4; }
-    while (e2 >= 3) { out.push_back(8); e2 -= 3; }
-    if (e2 == 2) out.push_back(4);
-    if (e2 == 1) out.push_back(2);
-    for (int p : {3, 5, 7})
-        while (m % p == 0) { out.push_back(p); m /= p; }
-    for (int64_t p = 11; m > 1; p += 2) {
-        if (p * p > m) p = m;   // m is prime now
-        while (m % p == 0) {
+    for (int64_t p = 2; p * p <= m; ++p)
+        while (m % p == 0) { f.push_back(p); m /= p; }
+    if (m > 1) f.push_back(m);
+    std::sort(f.rbegin(), f.rend());
+    // primes above 16 are stages of their own (generic radix, up to 61);
+    // the rest are packed greedily into compile-time radices of at most 16
+    std::vector<int64_t> small;
+    for (int64_t p : f) {
+        if (p > 16) {
             if (p > kGenericMaxRadix) return false;
             out.push_back(static_cast<int>(p));
-            m /= p;
+        } else {
+            small.push_back(p);
         }
+    }
+    while (!small.empty()) {
+        int64_t r = small.front();
+        small.erase(small.begin());
+        for (size_t i = 0; i < small.size();) {
+            if (r * small[i] <= 16) {
+                r *= small[i];
+                small.erase(small.begin() + static_cast<long>(i));
+            } else {
+                ++i;
+            }
+        }
+        out.push_back(static_cast<int>(r));
     }
     return static_cast<int>(out.size()) <= kMaxStages;
 }
@@ -111,12 +123,12 @@ struct FftRegistry {
         FftDesc d{};
         d.n = static_cast<int32_t>(n);
         d.nstages = static_cast<int32_t>(rad.size());
-        d.tw = static_cast<int32_t>(p.twpool.size() / 2);
         d.max_generic = 0;
         for (size_t s = 0; s < rad.size(); ++s) {
             d.radix[s] = static_cast<int16_t>(rad[s]);
-            if (rad[s] > 8) d.max_generic = std::max(d.max_generic, rad[s]);
+            if (rad[s] > 16) d.max_generic = std::max(d.max_generic, rad[s]);
         }
+        d.full = static_cast<int32_t>(p.twpool.size() / 2);
         for (int64_t t = 0; t < n; ++t) push_c(p.twpool, root(t, n));
         int lg = 0;
         while ((int64_t(1) << (2 * lg)) < n) ++lg;
@@ -124,6 +136,21 @@ struct FftRegistry {
         d.nhi = static_cast<int32_t>((n + (int64_t(1) << lg) - 1) >> lg);
         for (int64_t i = 0; i < d.nhi; ++i) push_c(p.twpool, root(i << lg, n));
         for (int64_t j = 0; j < (int64_t(1) << lg); ++j) push_c(p.twpool, root(j, n));
+        // stage twiddles omega_{Ns R}^{r k} = omega_n^{r k n / (Ns R)}
+        d.stw = static_cast<int32_t>(p.twpool.size() / 2);
+        int64_t Ns = 1, off = 0;
+        for (size_t s = 0; s < rad.size(); ++s) {
+            const int64_t R = rad[s];
+            d.stoff[s] = static_cast<int32_t>(off);
+            if (s > 0) {
+                const int64_t stride = n / (Ns * R);
+                for (int64_t k = 0; k < Ns; ++k)
+                    for (int64_t r = 1; r < R; ++r) push_c(p.twpool, root(r * k * stride, n));
+                off += (R - 1) * Ns;
+            }
+            Ns *= R;
+        }
+        d.ntw = static_cast<int32_t>(off);
         p.ffts.push_back(d);
         const int id = static_cast<int>(p.ffts.size()) - 1;
         index[n] = id;
@@ -298,23 +325,28 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         if (f.L2 > 8192) return fail(err, NSGCQT_EUNSUPPORTED, "packed length too large for the two-pass FFT");
         f.fft1 = reg.get(f.L1);
         f.fft2 = reg.get(f.L2);
-        auto pick = [](int64_t n, int& tile, int& nt) {
-            // up to 16 transforms per workgroup, at most 8 elements per thread
-            for (int t : {256, 512, 1024}) {
-                if (16 * n <= 8 * t) { tile = 16; nt = t; return; }
-            }
+        // up to 16 sequences per workgroup (a power of two), at most 8
+        // elements per thread
+        auto pick = [](int64_t n, int64_t count, int& lgt, int& nt) {
+            lgt = 4;
+            while (lgt > 0 && ((int64_t(1) << lgt) * n > 8192 || (int64_t(1) << (lgt - 1)) >= count)) --lgt;
             nt = 1024;
-            tile = static_cast<int>(std::max<int64_t>(1, 8 * 1024 / n));
+            for (int t : {256, 512, 1024})
+                if ((int64_t(1) << lgt) * n <= 8 * t) { nt = t; break; }
         };
-        pick(f.L1, f.tile_a, f.nt_a);
-        pick(f.L2, f.tile_b, f.nt_b);
-        f.tile_a = static_cast<int>(std::min<int64_t>(f.tile_a, f.L2));
-        f.tile_b = static_cast<int>(std::min<int64_t>(f.tile_b, f.L1));
-        f.ld_a = static_cast<int>(f.L1 | 1);
-        f.ld_b = static_cast<int>(f.L2 | 1);
-        if (static_cast<int64_t>(lds_slots(f.tile_a * f.ld_a)) * 8 > 160 * 1024 - 1024 ||
-            static_cast<int64_t>(lds_slots(f.tile_b * f.ld_b)) * 8 > 160 * 1024 - 1024)
-            return fail(err, NSGCQT_EUNSUPPORTED, "four-step tile exceeds LDS");
+        pick(f.L1, f.L2, f.tile_a, f.nt_a);
+        pick(f.L2, f.L1, f.tile_b, f.nt_b);
+        if ((int64_t(1) << f.tile_a) * f.L1 > 8192 || (int64_t(1) << f.tile_b) * f.L2 > 8192)
+            return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds one workgroup");
+        {
+            int lg4 = 0;
+            while ((int64_t(1) << (2 * lg4)) < L) ++lg4;
+            const int64_t t4 = ((L + (int64_t(1) << lg4) - 1) >> lg4) + (int64_t(1) << lg4);
+            const int64_t a_slots = kWrSlots + p.ffts[f.fft1].ntw + t4 + lds_slots(static_cast<int>(f.L1), f.tile_a);
+            const int64_t b_slots = kWrSlots + p.ffts[f.fft2].ntw + lds_slots(static_cast<int>(f.L2), f.tile_b);
+            if (a_slots * 8 > 160 * 1024 || b_slots * 8 > 160 * 1024)
+                return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds LDS");
+        }
         int lg = 0;
         while ((int64_t(1) << (2 * lg)) < L) ++lg;
         const int64_t s = int64_t(1) << lg;
@@ -371,7 +403,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
 
     // ---- buckets by transform length
     struct Tier { int max_work, nt, ept; };
-    const Tier tiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}, {16384, 1024, 16}};
+    const Tier tiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}};
     p.buckets.clear();
     for (const auto& t : tiers) {
         Bucket bk{};
@@ -382,7 +414,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     int big_t4 = 0, big_ea = 0, big_eb = 0;
     for (size_t l = 0; l < p.bands.size(); ++l) {
         int ti = -1;
-        for (int i = 0; i < 5; ++i)
+        for (int i = 0; i < 4; ++i)
             if (work[l] <= tiers[i].max_work) { ti = i; break; }
         if (ti < 0) {
             // four-step through global memory: n = n1 n2, n1 <= n2 <= 4096
@@ -406,18 +438,18 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             g.fft2 = reg.get(g.n2);
             if (g.fftn < 0 || g.fft1 < 0 || g.fft2 < 0)
                 return fail(err, NSGCQT_EUNSUPPORTED, "huge band transform has no radix plan");
-            g.tile_a = std::max(1, std::min<int>(16, std::min<int>(4096 / g.n1, g.n2)));
-            g.tile_b = std::max(1, std::min<int>(16, std::min<int>(4096 / g.n2, g.n1)));
-            g.ld_a = g.n1 | 1;
-            g.ld_b = g.n2 | 1;
+            g.lga = 4;
+            while (g.lga > 0 && ((1 << g.lga) * g.n1 > 4096 || (1 << (g.lga - 1)) >= g.n2)) --g.lga;
+            g.lgb = 4;
+            while (g.lgb > 0 && ((1 << g.lgb) * g.n2 > 4096 || (1 << (g.lgb - 1)) >= g.n1)) --g.lgb;
             g.hoff = static_cast<int32_t>(p.Hn);
             p.Hn += n;
             p.C_big += p.bands[l].M;
             if (p.banddev[l].chirp >= 0) { p.Hn_blu += n; p.C_big_blu += p.bands[l].M; }
             const FftDesc& fn = p.ffts[g.fftn];
             big_t4 = std::max(big_t4, fn.nhi + (1 << fn.lg));
-            big_ea = std::max(big_ea, g.tile_a * g.ld_a);
-            big_eb = std::max(big_eb, g.tile_b * g.ld_b);
+            big_ea = std::max(big_ea, lds_slots(g.n1, g.lga) + p.ffts[g.fft1].ntw);
+            big_eb = std::max(big_eb, lds_slots(g.n2, g.lgb) + p.ffts[g.fft2].ntw);
             p.bigs.push_back(g);
             continue;
         }
@@ -438,12 +470,18 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         bk.lds_elems = 0;
         for (int32_t l : bk.bands) {
             const int n = work[l];
-            const int G = std::max(1, std::min(batch, E / n));
-            bk.lds_elems = std::max(bk.lds_elems, G * n);
+            // 2^lg interleaved signals: at most 16, within E elements, and no
+            // more than the batch needs
+            int lg = 4;
+            while (lg > 0 && ((1 << lg) * n > E || (1 << (lg - 1)) >= batch)) --lg;
+            const int G = 1 << lg;
+            bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg) + p.ffts[p.banddev[l].fft].ntw);
             for (int s0 = 0; s0 < batch; s0 += G)
-                p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), 0});
+                p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), lg});
         }
         bk.nitems = static_cast<int>(p.items.size()) - bk.item_off;
+        if ((kWrSlots + bk.lds_elems) * 8 > 160 * 1024)
+            return fail(err, NSGCQT_EUNSUPPORTED, "band kernel exceeds LDS");
     }
 
     // huge-band work items: pass 0/1 over every huge band, pass 2/3 over the
@@ -453,14 +491,14 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         for (size_t gi = 0; gi < p.bigs.size(); ++gi) {
             const BigDesc& g = p.bigs[gi];
             if (pass >= 2 && p.banddev[g.band].chirp < 0) continue;
-            const int tiles = (pass % 2 == 0) ? (g.n2 + g.tile_a - 1) / g.tile_a : (g.n1 + g.tile_b - 1) / g.tile_b;
+            const int tiles = (pass % 2 == 0) ? (g.n2 + (1 << g.lga) - 1) >> g.lga : (g.n1 + (1 << g.lgb) - 1) >> g.lgb;
             for (int sg = 0; sg < batch; ++sg)
                 for (int t = 0; t < tiles; ++t) p.bigitems.push_back(BigItem{static_cast<int32_t>(gi), sg, t, 0});
         }
         p.big_n[pass] = static_cast<int>(p.bigitems.size()) - p.big_off[pass];
     }
-    p.big_lds_a = static_cast<int>((kWrSlots + kTwSlots + big_t4 + lds_slots(big_ea)) * 8);
-    p.big_lds_b = static_cast<int>((kWrSlots + kTwSlots + lds_slots(big_eb)) * 8);
+    p.big_lds_a = static_cast<int>((kWrSlots + big_t4 + big_ea) * 8);
+    p.big_lds_b = static_cast<int>((kWrSlots + big_eb) * 8);
     if (!p.bigs.empty() && (p.big_lds_a > 160 * 1024 || p.big_lds_b > 160 * 1024))
         return fail(err, NSGCQT_EUNSUPPORTED, "huge-band pass exceeds LDS");
 

@@ -27,18 +27,17 @@ struct Bucket {
     std::vector<int32_t> bands;
     int item_off;         // first work item of the bucket in HostPlan::items
     int nitems;
-    int lds_elems;        // largest count * transform length over its items
+    int lds_elems;        // largest data + stage-twiddle LDS slots over its items
 };
 
 // Four-step split of the packed FFT: L = L1 * L2. Pass A transforms columns
-// (length L1, `tile_a` columns per workgroup), pass B rows (length L2,
-// `tile_b` rows per workgroup).
+// (length L1, 2^tile_a columns per workgroup), pass B rows (length L2,
+// 2^tile_b rows per workgroup).
 struct FourStep {
     int64_t L1, L2;
     int fft1, fft2;       // FftDesc indices
-    int tile_a, tile_b;
+    int tile_a, tile_b;   // log2 of the sequences per workgroup
     int nt_a, nt_b;       // threads per workgroup of each pass
-    int ld_a, ld_b;       // LDS leading dimensions (padded)
     int64_t split;        // omega_L^t = hi[t >> split] * lo[t & (2^split - 1)]
 };
 

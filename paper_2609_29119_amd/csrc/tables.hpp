@@ -10,25 +10,27 @@ namespace nsg {
 // larger prime factor are transformed with Bluestein's chirp-z algorithm over a
 // 7-smooth length P >= 2M - 1.
 constexpr int kGenericMaxRadix = 61;
-constexpr int kMaxStages = 28;
+constexpr int kMaxStages = 24;
 
 // One transform length n: Stockham stages of the given radices, applied in
-// order, and the offset of its twiddles omega_n^t = exp(-2 pi i t / n),
-// t = 0..n-1, in the twiddle pool.
+// order. Twiddle pool layout per length: the full table omega_n^t (t < n) at
+// `full`, the two-level table (hi: nhi values, lo: 2^lg values) right after
+// it, and the stage twiddles at `stw`: for stage s >= 1 with radix R over
+// Ns = product of the earlier radices, omega_{Ns R}^{r k} at
+// stw + stoff[s] + k (R - 1) + r - 1 for k < Ns, 1 <= r < R (ntw values in all).
 struct FftDesc {
     int32_t n;
     int32_t nstages;
-    int32_t tw;
-    int32_t max_generic;     // largest generic (odd prime >= 11) radix, 0 if none
-    // two-level twiddles: omega_n^t = hi[t >> lg] * lo[t & (2^lg - 1)], with
-    // hi at tw + n (ceil(n / 2^lg) values) and lo right after it (2^lg values)
+    int32_t full;
     int32_t lg;
     int32_t nhi;
+    int32_t stw;
+    int32_t ntw;
+    int32_t max_generic;     // largest runtime (odd prime > 16) radix, 0 if none
     int16_t radix[kMaxStages];
+    int32_t stoff[kMaxStages];
 };
 
-// LDS slots reserved for the two-level twiddles of any length up to 16384.
-constexpr int kTwSlots = 288;
 // LDS slots reserved for the table of a generic odd-prime radix.
 constexpr int kWrSlots = 64;
 
@@ -44,12 +46,13 @@ struct BandDev {
     float inv_M;
 };
 
-// One workgroup of a band kernel: band `band` for signals s0 .. s0 + count - 1.
+// One workgroup of a band kernel: band `band` for signals s0 .. s0 + count - 1,
+// transformed as 2^lgnb interleaved sequences (count <= 2^lgnb).
 struct WorkItem {
     int32_t band;
     int32_t s0;
     int32_t count;
-    int32_t pad;
+    int32_t lgnb;
 };
 
 // A band whose transform (length M, or Bluestein P) exceeds one workgroup's
@@ -60,9 +63,9 @@ struct BigDesc {
     int32_t n, n1, n2;
     int32_t fftn;            // FftDesc of n: its tables give omega_n for the four-step twiddles
     int32_t fft1, fft2;      // FftDescs of the column (n1) and row (n2) transforms
-    int32_t tile_a, tile_b;  // columns / rows per workgroup
-    int32_t ld_a, ld_b;
+    int32_t lga, lgb;        // log2 of the columns / rows per workgroup
     int32_t hoff;
+    int32_t pad;
 };
 
 // One workgroup of a huge-band pass: band big, signal sig, tile index tile.
@@ -73,7 +76,7 @@ struct BigItem {
     int32_t pad;
 };
 
-// LDS slots holding n complex values under the padded index i + i/8.
-inline int lds_slots(int n) { return n + (n > 0 ? (n - 1) / 8 : 0) + 1; }
+// LDS slots of nb = 2^lgnb interleaved sequences of length n (stride nb + 1).
+inline int lds_slots(int n, int lgnb) { return lgnb ? n * ((1 << lgnb) + 1) : n; }
 
 }  // namespace nsg
