@@ -9,9 +9,9 @@
 // Each stage with radix R reads every butterfly's R inputs into registers,
 // multiplies them by the stage twiddles, applies a compile-time length-R DFT
 // and, after a barrier, writes the outputs in autosort order. The stage
-// twiddles omega_{Ns R}^{r k} are precomputed per transform length and copied
-// to LDS, R - 1 consecutive values per k, so a butterfly reads them with
-// immediate offsets. The caller guarantees nb * n <= NT * EPT.
+// twiddles omega_{Ns R}^{r k} are precomputed per transform length, R - 1
+// consecutive values per k, so a butterfly reads them with immediate offsets.
+// The caller guarantees nb * n <= NT * EPT.
 //
 // All transforms are forward DFTs (eq. 1, exp(-2 pi i k j / n)); inverse
 // transforms are obtained by conjugating input and output.
@@ -198,9 +198,10 @@ template <> struct Dft<16> { __device__ __forceinline__ static void run(float2* 
 // Butterfly jj of sequence t reads in[jj + r m] (m = n/R), multiplies input r
 // by omega_{Ns R}^{r k} (k = jj mod Ns, table tws[k (R-1) + r - 1]), applies
 // the length-R DFT, and after a barrier writes out[(jj - k) R + k + r Ns].
+// The twiddles omega_{Ns R}^{r k} come precomputed per stage (tws).
 template <int R, int NT, int EPT>
 __device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb, int Ns,
-                                            const float2* tws) {
+                                            const float2* __restrict__ tws) {
     constexpr int BPT = (EPT + R - 1) / R;
     const int tid = stage_tid();
     const int m = n / R;
@@ -255,7 +256,8 @@ __device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb,
 // DftPrime from s, d and the table wr[t] = omega_R^t.
 template <int NT, int EPT>
 __device__ __forceinline__ void stage_generic(float2* buf, int n, int S, int lgnb, int Ns, int R,
-                                              const float2* tws, float2* wr, const float2* __restrict__ full) {
+                                              const float2* __restrict__ tws, float2* wr,
+                                              const float2* __restrict__ full) {
     constexpr int IPT = (EPT + 4) / 5;   // items <= NT EPT (R + 7) / (8 R) <= 0.18 NT EPT
     const int tid = stage_tid();
     const int m = n / R;
@@ -353,21 +355,20 @@ __device__ __forceinline__ void stage_generic(float2* buf, int n, int S, int lgn
 }
 
 // Forward DFTs of nb = 2^lgnb sequences of length d->n, element i of
-// sequence t at buf[i S + t]. `wr` is LDS scratch for kWrSlots values and
-// `tws` for the d->ntw stage twiddles. The first stage (Ns = 1) needs no
-// twiddles and ends with a barrier, so the table copy made here is visible
-// from the second stage on. Ends with a barrier when there is a stage.
+// sequence t at buf[i S + t]. `wr` is LDS scratch for kWrSlots values; the
+// stage twiddles are read from the pool (each butterfly reads R - 1
+// consecutive values, shared by every workgroup of the same length, so they
+// stay in the caches). Ends with a barrier when there is a stage.
 template <int NT, int EPT>
 __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftDesc* __restrict__ d,
-                                        const float2* __restrict__ pool, float2* wr, float2* tws) {
+                                        const float2* __restrict__ pool, float2* wr) {
     const int n = d->n;
     const int ns = d->nstages;
-    for (int i = threadIdx.x; i < d->ntw; i += NT) tws[i] = pool[d->stw + i];
     const float2* full = pool + d->full;
     int Ns = 1;
     for (int s = 0; s < ns; ++s) {
         const int R = d->radix[s];
-        const float2* tw = tws + d->stoff[s];
+        const float2* tw = pool + d->stw + d->stoff[s];
         switch (R) {
             case 2: stage_fixed<2, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
             case 3: stage_fixed<3, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;

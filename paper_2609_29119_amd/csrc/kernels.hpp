@@ -67,13 +67,12 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
     return x * q + (x < r ? x : r) + i;
 }
 
-// LDS of the pass kernels: generic radix table, stage twiddles, four-step
-// twiddles (hi then lo, pass A only), data.
-__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_tw4, float2*& wr, float2*& tws,
-                                         float2*& t4, float2*& buf) {
+// LDS of the pass kernels: generic radix table, four-step twiddles (hi then
+// lo, pass A only), data.
+__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_tw4, float2*& wr, float2*& t4,
+                                         float2*& buf) {
     wr = lds;
-    tws = wr + kWrSlots;
-    t4 = tws + p.ntw;
+    t4 = wr + kWrSlots;
     buf = t4 + (with_tw4 ? p.nhi4 + (1 << p.split) : 0);
 }
 
@@ -95,8 +94,8 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
                                                       Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
     extern __shared__ float2 lds[];
-    float2 *wr, *tws, *t4, *buf;
-    pass_lds(lds, p, true, wr, tws, t4, buf);
+    float2 *wr, *t4, *buf;
+    pass_lds(lds, p, true, wr, t4, buf);
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
@@ -129,7 +128,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
         }
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
@@ -160,8 +159,8 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
                                                       Pass p, Tables T, int batch, long long C) {
     extern __shared__ float2 lds[];
-    float2 *wr, *tws, *t4, *buf;
-    pass_lds(lds, p, true, wr, tws, t4, buf);
+    float2 *wr, *t4, *buf;
+    pass_lds(lds, p, true, wr, t4, buf);
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
@@ -188,7 +187,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
         buf[__mul24(n1, S) + c] = v;
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
@@ -209,8 +208,8 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
                                                        Pass p, Tables T, int batch, long long out_stride,
                                                        float inv_L) {
     extern __shared__ float2 lds[];
-    float2 *wr, *tws, *t4, *buf;
-    pass_lds(lds, p, false, wr, tws, t4, buf);
+    float2 *wr, *t4, *buf;
+    pass_lds(lds, p, false, wr, t4, buf);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
@@ -226,7 +225,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
         buf[__mul24(n2, S) + r] = r < rows ? Ys[e] : make_float2(0.f, 0.f);
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
     float2* os = out + (long long)sig * out_stride;
     for (int e = threadIdx.x; e < tot; e += NT) {
         const int r = e & nbm, k2 = e >> p.lgnb;
@@ -259,8 +258,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
     float2* wr = lds;
-    float2* tws = wr + kWrSlots;
-    float2* buf = tws + fd->ntw;
+    float2* buf = wr + kWrSlots;
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
@@ -292,7 +290,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     if (blu) {
         const float2* K = T.kern + bd.kern;
         for (int e = threadIdx.x; e < (n << lg); e += NT) {
@@ -301,7 +299,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
             buf[a] = conjf2(cmul(buf[a], K[i]));
         }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
+        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     }
     const float2* ch = T.chirp + (blu ? bd.chirp : 0);
     for (int e = threadIdx.x; e < __mul24(g, M); e += NT) {
@@ -330,8 +328,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
     float2* wr = lds;
-    float2* tws = wr + kWrSlots;
-    float2* buf = tws + fd->ntw;
+    float2* buf = wr + kWrSlots;
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
@@ -351,7 +348,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     if (blu) {
         const float2* K = T.kern + bd.kern;
         for (int e = threadIdx.x; e < (n << lg); e += NT) {
@@ -360,7 +357,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
             buf[a] = conjf2(cmul(buf[a], K[i]));
         }
         __syncthreads();
-        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr, tws);
+        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     }
     const float* w = wt + bd.off;
     for (int e = threadIdx.x; e < __mul24(g, M); e += NT) {
@@ -411,8 +408,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
     float2* wr = lds;
     float2* t4 = wr + kWrSlots;
     const int nt4 = fdn->nhi + (1 << fdn->lg);
-    float2* tws = t4 + nt4;
-    float2* buf = tws + fd1->ntw;
+    float2* buf = t4 + nt4;
     for (int i = threadIdx.x; i < nt4; i += NT) t4[i] = T.tw[fdn->full + fdn->n + i];
     const TwL w4{t4, fdn->nhi, fdn->lg};
     const int M = bd.M;
@@ -453,7 +449,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
         buf[__mul24(r, S) + c] = v;
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd1, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, lg, fd1, T.tw, wr);
     __syncthreads();
     float2* Y = a.H1 + hbase;
     for (int e = threadIdx.x; e < tot; e += NT) {
@@ -476,8 +472,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int i
     const BandDev bd = T.bands[bg.band];
     const FftDesc* fd2 = T.ffts + bg.fft2;
     float2* wr = lds;
-    float2* tws = wr + kWrSlots;
-    float2* buf = tws + fd2->ntw;
+    float2* buf = wr + kWrSlots;
     const int M = bd.M;
     const bool blu = bd.chirp >= 0;
     const int lg = bg.lgb, nbm = (1 << lg) - 1, S = seq_stride(lg);
@@ -493,7 +488,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int i
         buf[__mul24(c, S) + r] = r < rows ? Y[e] : make_float2(0.f, 0.f);
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd2, T.tw, wr, tws);
+    lds_fft<NT, EPT>(buf, S, lg, fd2, T.tw, wr);
     const bool to_mid = blu && !second;
     for (int e = threadIdx.x; e < tot; e += NT) {
         const int r = e & nbm, k2 = e >> lg;

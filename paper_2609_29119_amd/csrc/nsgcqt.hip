@@ -147,10 +147,10 @@ Pass pass_b(const HostPlan& h) {
 }
 
 int lds_pass_a(const Pass& q) {
-    return (kWrSlots + q.ntw + q.nhi4 + (1 << q.split) + lds_slots(q.L1, q.lgnb)) * static_cast<int>(sizeof(float2));
+    return (kWrSlots + q.nhi4 + (1 << q.split) + lds_slots(q.L1, q.lgnb)) * static_cast<int>(sizeof(float2));
 }
 int lds_pass_b(const Pass& q) {
-    return (kWrSlots + q.ntw + lds_slots(q.L2, q.lgnb)) * static_cast<int>(sizeof(float2));
+    return (kWrSlots + lds_slots(q.L2, q.lgnb)) * static_cast<int>(sizeof(float2));
 }
 
 #define DISPATCH_NT(nt, KERNEL, ...)                                                         \

@@ -342,8 +342,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             int lg4 = 0;
             while ((int64_t(1) << (2 * lg4)) < L) ++lg4;
             const int64_t t4 = ((L + (int64_t(1) << lg4) - 1) >> lg4) + (int64_t(1) << lg4);
-            const int64_t a_slots = kWrSlots + p.ffts[f.fft1].ntw + t4 + lds_slots(static_cast<int>(f.L1), f.tile_a);
-            const int64_t b_slots = kWrSlots + p.ffts[f.fft2].ntw + lds_slots(static_cast<int>(f.L2), f.tile_b);
+            const int64_t a_slots = kWrSlots + t4 + lds_slots(static_cast<int>(f.L1), f.tile_a);
+            const int64_t b_slots = kWrSlots + lds_slots(static_cast<int>(f.L2), f.tile_b);
             if (a_slots * 8 > 160 * 1024 || b_slots * 8 > 160 * 1024)
                 return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds LDS");
         }
@@ -448,8 +448,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             if (p.banddev[l].chirp >= 0) { p.Hn_blu += n; p.C_big_blu += p.bands[l].M; }
             const FftDesc& fn = p.ffts[g.fftn];
             big_t4 = std::max(big_t4, fn.nhi + (1 << fn.lg));
-            big_ea = std::max(big_ea, lds_slots(g.n1, g.lga) + p.ffts[g.fft1].ntw);
-            big_eb = std::max(big_eb, lds_slots(g.n2, g.lgb) + p.ffts[g.fft2].ntw);
+            big_ea = std::max(big_ea, lds_slots(g.n1, g.lga));
+            big_eb = std::max(big_eb, lds_slots(g.n2, g.lgb));
             p.bigs.push_back(g);
             continue;
         }
@@ -475,7 +475,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             int lg = 4;
             while (lg > 0 && ((1 << lg) * n > E || (1 << (lg - 1)) >= batch)) --lg;
             const int G = 1 << lg;
-            bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg) + p.ffts[p.banddev[l].fft].ntw);
+            bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg));
             for (int s0 = 0; s0 < batch; s0 += G)
                 p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), lg});
         }

@@ -27,7 +27,7 @@ struct Bucket {
     std::vector<int32_t> bands;
     int item_off;         // first work item of the bucket in HostPlan::items
     int nitems;
-    int lds_elems;        // largest data + stage-twiddle LDS slots over its items
+    int lds_elems;        // largest data LDS slots over its items
 };
 
 // Four-step split of the packed FFT: L = L1 * L2. Pass A transforms columns
