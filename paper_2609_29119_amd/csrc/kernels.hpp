@@ -30,6 +30,7 @@ struct Tables {
     const float2* omega;     // exp(-2 pi i k / N), k = 0..L
     const int32_t* owner;    // first band covering bin k | count << 24, k = 0..L
     const int32_t* bandbase; // off - k_lo per band
+    const int4* gather;      // per bin k = 0..L: W indices of up to 3 covering bands, count
     const float2* chirp;     // Bluestein exp(-i pi m^2 / M)
     const float2* kern;      // Bluestein DFT_P(b) / P
     const float2* tw4_hi;
@@ -140,12 +141,13 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
     }
 }
 
-// X_q = sum of the weighted band spectra W over the bands covering bin q.
+// X_q = sum of the weighted band spectra W over the (at most three) bands
+// covering bin q; the bin's record holds their W indices and count.
 __device__ __forceinline__ float2 gather_bin(const Tables& T, const float2* __restrict__ Ws, int q) {
-    const int o = T.owner[q];
-    const int first = o & 0xFFFFFF, cnt = o >> 24;
-    float2 acc = make_float2(0.f, 0.f);
-    for (int i = 0; i < cnt; ++i) acc = cadd(acc, Ws[T.bandbase[first + i] + q]);
+    const int4 g = T.gather[q];
+    float2 acc = Ws[g.x];
+    if (g.w > 1) acc = cadd(acc, Ws[g.y]);
+    if (g.w > 2) acc = cadd(acc, Ws[g.z]);
     return acc;
 }
 

@@ -67,6 +67,7 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iOm = add(h.omega.data(), h.omega.size() * sizeof(float));
     const size_t iOwn = add(h.owner.data(), h.owner.size() * sizeof(int32_t));
     const size_t iBase = add(h.bandbase.data(), h.bandbase.size() * sizeof(int32_t));
+    const size_t iGather = add(h.gather.data(), h.gather.size() * sizeof(int32_t));
     const size_t iCh = add(h.chirp.data(), h.chirp.size() * sizeof(float));
     const size_t iK = add(h.kern.data(), h.kern.size() * sizeof(float));
     const size_t iHi = add(h.tw4_hi.data(), h.tw4_hi.size() * sizeof(float));
@@ -95,6 +96,7 @@ int upload(nsgcqt_plan_s* p) {
     T.omega = static_cast<const float2*>(at(iOm));
     T.owner = static_cast<const int32_t*>(at(iOwn));
     T.bandbase = static_cast<const int32_t*>(at(iBase));
+    T.gather = static_cast<const int4*>(at(iGather));
     T.chirp = static_cast<const float2*>(at(iCh));
     T.kern = static_cast<const float2*>(at(iK));
     T.tw4_hi = static_cast<const float2*>(at(iHi));

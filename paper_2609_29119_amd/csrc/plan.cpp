@@ -301,6 +301,15 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     p.bandbase.resize(p.bands.size());
     for (size_t l = 0; l < p.bands.size(); ++l)
         p.bandbase[l] = static_cast<int32_t>(p.bands[l].off - p.bands[l].k_lo);
+    // per bin: the W indices (within one signal's row) of the covering bands
+    // and their count, so the overlap-add reads W after one table load
+    if (p.max_overlap > 3) return fail(err, NSGCQT_EUNSUPPORTED, "more than three bands cover one bin");
+    p.gather.assign(4 * (half + 1), 0);
+    for (int64_t k = 0; k <= half; ++k) {
+        const int first = p.owner[k] & 0xFFFFFF, cnt = p.owner[k] >> 24;
+        for (int j = 0; j < cnt; ++j) p.gather[4 * k + j] = static_cast<int32_t>(p.bandbase[first + j] + k);
+        p.gather[4 * k + 3] = cnt;
+    }
 
     // ---- omega_k = exp(-2 pi i k / N) for the untangle (eq. 6) and retangle (eq. 9)
     p.omega.clear();
