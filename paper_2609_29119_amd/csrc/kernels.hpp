@@ -68,6 +68,25 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
     return x * q + (x < r ? x : r) + i;
 }
 
+// Load phase shared by the kernels: thread tid takes the elements
+// e = tid + j NT < total, U at a time. get(e) performs the element's global
+// reads and touches only valid addresses for every 0 <= e < total (callers
+// clamp indices and mask the value in put); put(e, v) consumes them. All U
+// gets are issued before the first put, so a wave keeps U elements' reads in
+// flight instead of waiting for each element in turn.
+template <int NT, int U, class Get, class Put>
+__device__ __forceinline__ void load_phase(int total, Get get, Put put) {
+    using V = decltype(get(0));
+    for (int base = threadIdx.x; base < total; base += U * NT) {
+        V v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = get(min(base + u * NT, total - 1));
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (base + u * NT < total) put(base + u * NT, v[u]);
+    }
+}
+
 // LDS of the pass kernels: generic radix table, four-step twiddles (hi then
 // lo, pass A only), data.
 __device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_tw4, float2*& wr, float2*& t4,
@@ -79,8 +98,10 @@ __device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_t
 
 template <int NT>
 __device__ __forceinline__ void load_tw4(float2* t4, const Pass& p, const Tables& T) {
-    for (int i = threadIdx.x; i < p.nhi4; i += NT) t4[i] = T.tw4_hi[i];
-    for (int i = threadIdx.x; i < (1 << p.split); i += NT) t4[p.nhi4 + i] = T.tw4_lo[i];
+    const int nlo = 1 << p.split;
+    load_phase<NT, 2>(
+        p.nhi4 + nlo, [&](int i) { return *(i < p.nhi4 ? T.tw4_hi + i : T.tw4_lo + (i - p.nhi4)); },
+        [&](int i, float2 v) { t4[i] = v; });
 }
 
 __device__ __forceinline__ float2 tw4(const float2* t4, const Pass& p, int t) {
@@ -107,26 +128,38 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
     const int tot = p.L1 << p.lgnb;
     if (!sl.enabled) {
         const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
-        for (int e = threadIdx.x; e < tot; e += NT) {
-            const int c = e & nbm, n1 = e >> p.lgnb;
-            buf[__mul24(n1, S) + c] = c < cols ? z[__mul24(n1, p.L2) + n2a + c] : make_float2(0.f, 0.f);
-        }
+        load_phase<NT, 4>(
+            tot,
+            [&](int e) { return z[__mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1)]; },
+            [&](int e, float2 v) {
+                const int c = e & nbm;
+                buf[__mul24(e >> p.lgnb, S) + c] = c < cols ? v : make_float2(0.f, 0.f);
+            });
     } else {
         // padded coordinate of sample 2j of slice s is s H + 2j; the signal
-        // starts at padded H
+        // starts at padded H. Reads are clamped into the signal and masked.
         const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
-        for (int e = threadIdx.x; e < tot; e += NT) {
-            const int c = e & nbm, n1 = e >> p.lgnb;
-            float2 v = make_float2(0.f, 0.f);
-            if (c < cols) {
+        const long long last = sl.n - 1;
+        load_phase<NT, 4>(
+            tot,
+            [&](int e) {
+                const int j = __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1);
+                const long long t = base + 2 * (long long)j;
+                const long long t0 = t < 0 ? 0 : (t > last ? last : t);
+                const long long t1 = t + 1 < 0 ? 0 : (t + 1 > last ? last : t + 1);
+                return make_float4(x[t0], x[t1], T.slicewin[2 * j], T.slicewin[2 * j + 1]);
+            },
+            [&](int e, float4 r) {
+                const int c = e & nbm, n1 = e >> p.lgnb;
                 const int j = __mul24(n1, p.L2) + n2a + c;
                 const long long t = base + 2 * (long long)j;
-                const float v0 = (t >= 0 && t < sl.n) ? x[t] : 0.f;
-                const float v1 = (t + 1 >= 0 && t + 1 < sl.n) ? x[t + 1] : 0.f;
-                v = make_float2(v0 * T.slicewin[2 * j], v1 * T.slicewin[2 * j + 1]);
-            }
-            buf[__mul24(n1, S) + c] = v;
-        }
+                float2 v = make_float2(0.f, 0.f);
+                if (c < cols) {
+                    if (t >= 0 && t < sl.n) v.x = r.x * r.z;
+                    if (t + 1 >= 0 && t + 1 < sl.n) v.y = r.y * r.w;
+                }
+                buf[__mul24(n1, S) + c] = v;
+            });
     }
     __syncthreads();
     lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
@@ -142,13 +175,15 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
 }
 
 // X_q = sum of the weighted band spectra W over the (at most three) bands
-// covering bin q; the bin's record holds their W indices and count.
-__device__ __forceinline__ float2 gather_bin(const Tables& T, const float2* __restrict__ Ws, int q) {
-    const int4 g = T.gather[q];
-    float2 acc = Ws[g.x];
-    if (g.w > 1) acc = cadd(acc, Ws[g.y]);
-    if (g.w > 2) acc = cadd(acc, Ws[g.z]);
-    return acc;
+// covering bin q; the bin's record holds their W indices (unused ones 0, a
+// valid index) and count. All three reads are issued unconditionally.
+__device__ __forceinline__ float4 make_float4_2(float2 a, float2 b) { return make_float4(a.x, a.y, b.x, b.y); }
+
+__device__ __forceinline__ float2 gather_bin(const float2* __restrict__ Ws, int4 g) {
+    const float2 a = Ws[g.x], b = Ws[g.y], c = Ws[g.z];
+    // masks instead of branches, so the compiler cannot sink the reads
+    const float mb = g.w > 1 ? 1.f : 0.f, mc = g.w > 2 ? 1.f : 0.f;
+    return make_float2(a.x + mb * b.x + mc * c.x, a.y + mb * b.y + mc * c.y);
 }
 
 // ------------------------------- inverse packed FFT, pass A, with overlap-add
@@ -172,21 +207,42 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     const int cols = min(nbm + 1, p.L2 - n2a);
     const int tot = p.L1 << p.lgnb;
     const float2* Ws = W + (long long)sig * C;
-    for (int e = threadIdx.x; e < tot; e += NT) {
-        const int c = e & nbm, n1 = e >> p.lgnb;
-        float2 v = make_float2(0.f, 0.f);
-        if (c < cols) {
-            const int q = __mul24(n1, p.L2) + n2a + c;
-            float2 xq = gather_bin(T, Ws, q);
-            float2 xm = gather_bin(T, Ws, p.L - q);
-            if (q == 0) { xq.y = 0.f; xm.y = 0.f; }
-            const float2 om = T.omega[q];                         // (cos, -sin)
-            const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w)
-            const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
-            const float2 zq = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
-            v = make_float2(0.5f * zq.x, -0.5f * zq.y);           // conj(Z_q)
+    // U elements at a time: the bin records of q and L - q, then the W values
+    // they name, then the retangle; indices are clamped into the tile
+    constexpr int U = 4;
+    for (int base = threadIdx.x; base < tot; base += U * NT) {
+        int4 gq[U], gm[U];
+        float2 om[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = min(base + u * NT, tot - 1);
+            const int q = __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1);
+            gq[u] = T.gather[q];
+            gm[u] = T.gather[p.L - q];
+            om[u] = T.omega[q];                                   // (cos, -sin)
         }
-        buf[__mul24(n1, S) + c] = v;
+        float2 xq[U], xm[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            xq[u] = gather_bin(Ws, gq[u]);
+            xm[u] = gather_bin(Ws, gm[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int e = base + u * NT;
+            if (e < tot) {
+                const int c = e & nbm, n1 = e >> p.lgnb;
+                float2 v = make_float2(0.f, 0.f);
+                if (c < cols) {
+                    if (n1 == 0 && n2a + c == 0) { xq[u].y = 0.f; xm[u].y = 0.f; }
+                    const float2 pa = make_float2(1.f + om[u].y, om[u].x);    // 1 + i conj(w)
+                    const float2 pb = make_float2(1.f - om[u].y, -om[u].x);   // 1 - i conj(w)
+                    const float2 zq = cadd(cmul(pa, xq[u]), cmul(pb, conjf2(xm[u])));
+                    v = make_float2(0.5f * zq.x, -0.5f * zq.y);               // conj(Z_q)
+                }
+                buf[__mul24(n1, S) + c] = v;
+            }
+        }
     }
     __syncthreads();
     lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
@@ -221,11 +277,15 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
     const int tot = p.L2 << p.lgnb;
     const Div dl2 = mkdiv(p.L2);
     const float2* Ys = Y + (long long)sig * p.L + (long long)k1a * p.L2;
-    for (int e = threadIdx.x; e < tot; e += NT) {
-        int n2;
-        const int r = qdiv(e, dl2, n2);
-        buf[__mul24(n2, S) + r] = r < rows ? Ys[e] : make_float2(0.f, 0.f);
-    }
+    // rows past the last one are read clamped and stored as zeros
+    const int last = __mul24(rows, p.L2) - 1;
+    load_phase<NT, 4>(
+        tot, [&](int e) { return Ys[min(e, last)]; },
+        [&](int e, float2 v) {
+            int n2;
+            const int r = qdiv(e, dl2, n2);
+            buf[__mul24(n2, S) + r] = r < rows ? v : make_float2(0.f, 0.f);
+        });
     __syncthreads();
     lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
     float2* os = out + (long long)sig * out_stride;
@@ -266,28 +326,39 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
     const bool blu = bd.chirp >= 0;
     const float* w = wt + bd.off;
     const Div dM = mkdiv(M);
-    for (int e = threadIdx.x; e < (M << lg); e += NT) {
-        int i;
-        const int sg = qdiv(e, dM, i);
-        int slot = i + bd.rot;
-        if (slot >= M) slot -= M;
-        float2 v = make_float2(0.f, 0.f);
-        if (sg < g) {
-            const float2* Zs = Z + (long long)(it.s0 + sg) * L;
+    // reads of signals past the item's count are clamped to its first signal
+    // and their slots set to zero; the chirp index is 0 for non-Bluestein
+    // bands (every device table holds at least 256 bytes)
+    struct RouteIn { float2 za, zb, om, ch; float w; };
+    load_phase<NT, 4>(
+        M << lg,
+        [&](int e) {
+            int i;
+            const int sg = qdiv(e, dM, i);
+            int slot = i + bd.rot;
+            if (slot >= M) slot -= M;
+            const float2* Zs = Z + (long long)(it.s0 + (sg < g ? sg : 0)) * L;
             const int k = bd.k_lo + i;
             const int a = (k == L) ? 0 : k;
             const int bm = (a == 0) ? 0 : L - a;
-            const float2 za = Zs[a], zb = Zs[bm];
-            const float2 om = T.omega[k];                         // (cos, -sin)
-            const float2 pa = make_float2(1.f + om.y, -om.x);     // 1 - i w_k
-            const float2 pb = make_float2(1.f - om.y, om.x);      // 1 + i w_k
-            const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
-            const float hw = 0.5f * w[i];
-            v = make_float2(hw * u2.x, -hw * u2.y);               // conj(u)
-            if (blu) v = cmul(v, T.chirp[bd.chirp + slot]);
-        }
-        buf[__mul24(slot, S) + sg] = v;
-    }
+            return RouteIn{Zs[a], Zs[bm], T.omega[k], T.chirp[blu ? bd.chirp + slot : 0], w[i]};
+        },
+        [&](int e, const RouteIn& r) {
+            int i;
+            const int sg = qdiv(e, dM, i);
+            int slot = i + bd.rot;
+            if (slot >= M) slot -= M;
+            float2 v = make_float2(0.f, 0.f);
+            if (sg < g) {
+                const float2 pa = make_float2(1.f + r.om.y, -r.om.x);    // 1 - i w_k
+                const float2 pb = make_float2(1.f - r.om.y, r.om.x);     // 1 + i w_k
+                const float2 u2 = cadd(cmul(pa, r.za), cmul(pb, conjf2(r.zb)));
+                const float hw = 0.5f * r.w;
+                v = make_float2(hw * u2.x, -hw * u2.y);                  // conj(u)
+                if (blu) v = cmul(v, r.ch);
+            }
+            buf[__mul24(slot, S) + sg] = v;
+        });
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
@@ -295,23 +366,30 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
     lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     if (blu) {
         const float2* K = T.kern + bd.kern;
-        for (int e = threadIdx.x; e < (n << lg); e += NT) {
-            const int i = e >> lg;
-            const int a = __mul24(i, S) + (e & (nb - 1));
-            buf[a] = conjf2(cmul(buf[a], K[i]));
-        }
+        load_phase<NT, 4>(
+            n << lg, [&](int e) { return K[e >> lg]; },
+            [&](int e, float2 kv) {
+                const int a = __mul24(e >> lg, S) + (e & (nb - 1));
+                buf[a] = conjf2(cmul(buf[a], kv));
+            });
         __syncthreads();
         lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     }
-    const float2* ch = T.chirp + (blu ? bd.chirp : 0);
-    for (int e = threadIdx.x; e < __mul24(g, M); e += NT) {
-        int i;
-        const int sg = qdiv(e, dM, i);
-        const float2 v = buf[__mul24(i, S) + sg];
-        float2* cs = coef + (long long)(it.s0 + sg) * C + bd.off;
-        // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
-        cs[i] = blu ? cscale(cmul(conjf2(ch[i]), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
-    }
+    load_phase<NT, 4>(
+        __mul24(g, M),
+        [&](int e) {
+            int i;
+            qdiv(e, dM, i);
+            return T.chirp[blu ? bd.chirp + i : 0];
+        },
+        [&](int e, float2 chi) {
+            int i;
+            const int sg = qdiv(e, dM, i);
+            const float2 v = buf[__mul24(i, S) + sg];
+            float2* cs = coef + (long long)(it.s0 + sg) * C + bd.off;
+            // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
+            cs[i] = blu ? cscale(cmul(conjf2(chi), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+        });
 }
 
 // ----------------------------------------------------------- band synthesis
@@ -334,18 +412,26 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
-    const float2* ch = T.chirp + (blu ? bd.chirp : 0);
     const Div dM = mkdiv(M);
-    for (int e = threadIdx.x; e < (M << lg); e += NT) {
-        int i;
-        const int sg = qdiv(e, dM, i);
-        float2 v = make_float2(0.f, 0.f);
-        if (sg < g) {
-            v = coef[(long long)(it.s0 + sg) * C + bd.off + i];
-            if (blu) v = cmul(v, ch[i]);
-        }
-        buf[__mul24(i, S) + sg] = v;
-    }
+    // signals past the item's count read the first signal's row and store zeros
+    load_phase<NT, 4>(
+        M << lg,
+        [&](int e) {
+            int i;
+            const int sg = qdiv(e, dM, i);
+            return make_float4_2(coef[(long long)(it.s0 + (sg < g ? sg : 0)) * C + bd.off + i],
+                                 T.chirp[blu ? bd.chirp + i : 0]);
+        },
+        [&](int e, float4 r) {
+            int i;
+            const int sg = qdiv(e, dM, i);
+            float2 v = make_float2(0.f, 0.f);
+            if (sg < g) {
+                v = make_float2(r.x, r.y);
+                if (blu) v = cmul(v, make_float2(r.z, r.w));
+            }
+            buf[__mul24(i, S) + sg] = v;
+        });
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
@@ -353,24 +439,35 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
     lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     if (blu) {
         const float2* K = T.kern + bd.kern;
-        for (int e = threadIdx.x; e < (n << lg); e += NT) {
-            const int i = e >> lg;
-            const int a = __mul24(i, S) + (e & (nb - 1));
-            buf[a] = conjf2(cmul(buf[a], K[i]));
-        }
+        load_phase<NT, 4>(
+            n << lg, [&](int e) { return K[e >> lg]; },
+            [&](int e, float2 kv) {
+                const int a = __mul24(e >> lg, S) + (e & (nb - 1));
+                buf[a] = conjf2(cmul(buf[a], kv));
+            });
         __syncthreads();
         lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     }
     const float* w = wt + bd.off;
-    for (int e = threadIdx.x; e < __mul24(g, M); e += NT) {
-        int i;
-        const int sg = qdiv(e, dM, i);
-        int slot = i + bd.rot;
-        if (slot >= M) slot -= M;
-        float2 u = buf[__mul24(slot, S) + sg];
-        if (blu) u = cmul(ch[slot], conjf2(u));
-        W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, w[i]);
-    }
+    struct OutIn { float2 ch; float w; };
+    load_phase<NT, 4>(
+        __mul24(g, M),
+        [&](int e) {
+            int i;
+            qdiv(e, dM, i);
+            int slot = i + bd.rot;
+            if (slot >= M) slot -= M;
+            return OutIn{T.chirp[blu ? bd.chirp + slot : 0], w[i]};
+        },
+        [&](int e, const OutIn& r) {
+            int i;
+            const int sg = qdiv(e, dM, i);
+            int slot = i + bd.rot;
+            if (slot >= M) slot -= M;
+            float2 u = buf[__mul24(slot, S) + sg];
+            if (blu) u = cmul(r.ch, conjf2(u));
+            W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, r.w);
+        });
 }
 
 // ------------------------------------------------------------ huge bands
