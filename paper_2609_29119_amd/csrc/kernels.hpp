@@ -74,6 +74,16 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
 // clamp indices and mask the value in put); put(e, v) consumes them. All U
 // gets are issued before the first put, so a wave keeps U elements' reads in
 // flight instead of waiting for each element in turn.
+// Makes v's registers opaque: the loads producing v must complete here,
+// so the compiler cannot sink them into the (conditional) consumer.
+template <class V>
+__device__ __forceinline__ void pin(V& v) {
+    static_assert(sizeof(V) % 4 == 0, "pin expects 32-bit fields");
+    uint32_t* w = reinterpret_cast<uint32_t*>(&v);
+#pragma unroll
+    for (int i = 0; i < static_cast<int>(sizeof(V) / 4); ++i) asm volatile("" : "+v"(w[i]));
+}
+
 template <int NT, int U, class Get, class Put>
 __device__ __forceinline__ void load_phase(int total, Get get, Put put) {
     using V = decltype(get(0));
@@ -299,6 +309,51 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
 }
 
 // ------------------------------------------------------------ band analysis
+// Element idx of base through a 32-bit byte offset. With base uniform across
+// the wave this is the scalar-base + vector-offset address form, which saves
+// the 64-bit address arithmetic per access. The plan keeps every offset used
+// this way below 2^32 bytes.
+template <class T>
+__device__ __forceinline__ const T& at32(const T* base, uint32_t idx) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + idx * static_cast<uint32_t>(sizeof(T)));
+}
+template <class T>
+__device__ __forceinline__ T& at32(T* base, uint32_t idx) {
+    return *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + idx * static_cast<uint32_t>(sizeof(T)));
+}
+
+// Entries of nb = 2^lg interleaved sequences of length n: thread tid owns
+// sequence tid & (nb - 1) and its entries i = (tid >> lg) + j (NT >> lg) < n,
+// U at a time; as in load_phase, all U gets are issued before the first put,
+// and get only sees valid indices.
+template <int NT, int U, class Get, class Put>
+__device__ __forceinline__ void seq_phase(int n, int lg, Get get, Put put) {
+    const int step = NT >> lg;
+    using V = decltype(get(0));
+    for (int i0 = static_cast<int>(threadIdx.x) >> lg; i0 < n; i0 += U * step) {
+        V v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = get(min(i0 + u * step, n - 1));
+#pragma unroll
+        for (int u = 0; u < U; ++u) pin(v[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (i0 + u * step < n) put(i0 + u * step, v[u]);
+    }
+}
+
+// Bluestein's middle step on the LDS sequences: v <- conj(v K) for the
+// transformed kernel K (entries 0 .. n-1), sequence sg of this thread.
+template <int NT>
+__device__ __forceinline__ void blu_middle(float2* buf, int n, int lg, int S, int sg, const float2* K) {
+    seq_phase<NT, 4>(
+        n, lg, [&](int i) { return at32(K, i); },
+        [&](int i, float2 kv) {
+            const int a = __mul24(i, S) + sg;
+            buf[a] = conjf2(cmul(buf[a], kv));
+        });
+}
+
 // One workgroup per work item (band, signals s0 .. s0 + count - 1, interleaved
 // as 2^lgnb sequences). For entry i of the band (bin k = k_lo + i) the router
 // (eq. 7) forms
@@ -324,32 +379,31 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
+    // this thread's sequence; sequences past the item's count read signal 0
+    // and hold zeros
+    const int sg = threadIdx.x & (nb - 1);
+    const bool live = sg < g;
+    const float2* Zb = Z + (long long)it.s0 * L;
+    const uint32_t zrow = static_cast<uint32_t>(live ? sg : 0) * static_cast<uint32_t>(L);
+    const float2* chb = T.chirp + (blu ? bd.chirp : 0);   // entry 0 is valid in every table
     const float* w = wt + bd.off;
-    const Div dM = mkdiv(M);
-    // reads of signals past the item's count are clamped to its first signal
-    // and their slots set to zero; the chirp index is 0 for non-Bluestein
-    // bands (every device table holds at least 256 bytes)
     struct RouteIn { float2 za, zb, om, ch; float w; };
-    load_phase<NT, 4>(
-        M << lg,
-        [&](int e) {
-            int i;
-            const int sg = qdiv(e, dM, i);
+    seq_phase<NT, 4>(
+        M, lg,
+        [&](int i) {
             int slot = i + bd.rot;
             if (slot >= M) slot -= M;
-            const float2* Zs = Z + (long long)(it.s0 + (sg < g ? sg : 0)) * L;
             const int k = bd.k_lo + i;
             const int a = (k == L) ? 0 : k;
             const int bm = (a == 0) ? 0 : L - a;
-            return RouteIn{Zs[a], Zs[bm], T.omega[k], T.chirp[blu ? bd.chirp + slot : 0], w[i]};
+            return RouteIn{at32(Zb, zrow + a), at32(Zb, zrow + bm), at32(T.omega, k), at32(chb, blu ? slot : 0),
+                           at32(w, i)};
         },
-        [&](int e, const RouteIn& r) {
-            int i;
-            const int sg = qdiv(e, dM, i);
+        [&](int i, const RouteIn& r) {
             int slot = i + bd.rot;
             if (slot >= M) slot -= M;
             float2 v = make_float2(0.f, 0.f);
-            if (sg < g) {
+            if (live) {
                 const float2 pa = make_float2(1.f + r.om.y, -r.om.x);    // 1 - i w_k
                 const float2 pb = make_float2(1.f - r.om.y, r.om.x);     // 1 + i w_k
                 const float2 u2 = cadd(cmul(pa, r.za), cmul(pb, conjf2(r.zb)));
@@ -365,30 +419,20 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
     __syncthreads();
     lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     if (blu) {
-        const float2* K = T.kern + bd.kern;
-        load_phase<NT, 4>(
-            n << lg, [&](int e) { return K[e >> lg]; },
-            [&](int e, float2 kv) {
-                const int a = __mul24(e >> lg, S) + (e & (nb - 1));
-                buf[a] = conjf2(cmul(buf[a], kv));
-            });
+        blu_middle<NT>(buf, n, lg, S, sg, T.kern + bd.kern);
         __syncthreads();
         lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     }
-    load_phase<NT, 4>(
-        __mul24(g, M),
-        [&](int e) {
-            int i;
-            qdiv(e, dM, i);
-            return T.chirp[blu ? bd.chirp + i : 0];
-        },
-        [&](int e, float2 chi) {
-            int i;
-            const int sg = qdiv(e, dM, i);
+    if (!live) return;
+    float2* cb = coef + (long long)it.s0 * C + bd.off;
+    const uint32_t crow = static_cast<uint32_t>(sg) * static_cast<uint32_t>(C);
+    seq_phase<NT, 4>(
+        M, lg, [&](int i) { return at32(chb, blu ? i : 0); },
+        [&](int i, float2 chi) {
             const float2 v = buf[__mul24(i, S) + sg];
-            float2* cs = coef + (long long)(it.s0 + sg) * C + bd.off;
             // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
-            cs[i] = blu ? cscale(cmul(conjf2(chi), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+            at32(cb, crow + i) =
+                blu ? cscale(cmul(conjf2(chi), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
         });
 }
 
@@ -412,21 +456,16 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
-    const Div dM = mkdiv(M);
-    // signals past the item's count read the first signal's row and store zeros
-    load_phase<NT, 4>(
-        M << lg,
-        [&](int e) {
-            int i;
-            const int sg = qdiv(e, dM, i);
-            return make_float4_2(coef[(long long)(it.s0 + (sg < g ? sg : 0)) * C + bd.off + i],
-                                 T.chirp[blu ? bd.chirp + i : 0]);
-        },
-        [&](int e, float4 r) {
-            int i;
-            const int sg = qdiv(e, dM, i);
+    const int sg = threadIdx.x & (nb - 1);
+    const bool live = sg < g;
+    const float2* chb = T.chirp + (blu ? bd.chirp : 0);   // entry 0 is valid in every table
+    const float2* cb = coef + (long long)it.s0 * C + bd.off;
+    const uint32_t crow = static_cast<uint32_t>(live ? sg : 0) * static_cast<uint32_t>(C);
+    seq_phase<NT, 4>(
+        M, lg, [&](int i) { return make_float4_2(at32(cb, crow + i), at32(chb, blu ? i : 0)); },
+        [&](int i, float4 r) {
             float2 v = make_float2(0.f, 0.f);
-            if (sg < g) {
+            if (live) {
                 v = make_float2(r.x, r.y);
                 if (blu) v = cmul(v, make_float2(r.z, r.w));
             }
@@ -438,35 +477,27 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
     __syncthreads();
     lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     if (blu) {
-        const float2* K = T.kern + bd.kern;
-        load_phase<NT, 4>(
-            n << lg, [&](int e) { return K[e >> lg]; },
-            [&](int e, float2 kv) {
-                const int a = __mul24(e >> lg, S) + (e & (nb - 1));
-                buf[a] = conjf2(cmul(buf[a], kv));
-            });
+        blu_middle<NT>(buf, n, lg, S, sg, T.kern + bd.kern);
         __syncthreads();
         lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
     }
+    if (!live) return;
     const float* w = wt + bd.off;
+    float2* Wb = W + (long long)it.s0 * C + bd.off;
     struct OutIn { float2 ch; float w; };
-    load_phase<NT, 4>(
-        __mul24(g, M),
-        [&](int e) {
-            int i;
-            qdiv(e, dM, i);
+    seq_phase<NT, 4>(
+        M, lg,
+        [&](int i) {
             int slot = i + bd.rot;
             if (slot >= M) slot -= M;
-            return OutIn{T.chirp[blu ? bd.chirp + slot : 0], w[i]};
+            return OutIn{at32(chb, blu ? slot : 0), at32(w, i)};
         },
-        [&](int e, const OutIn& r) {
-            int i;
-            const int sg = qdiv(e, dM, i);
+        [&](int i, const OutIn& r) {
             int slot = i + bd.rot;
             if (slot >= M) slot -= M;
             float2 u = buf[__mul24(slot, S) + sg];
             if (blu) u = cmul(r.ch, conjf2(u));
-            W[(long long)(it.s0 + sg) * C + bd.off + i] = cscale(u, r.w);
+            at32(Wb, crow + i) = cscale(u, r.w);
         });
 }
 

@@ -177,8 +177,10 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     if (batch < 1) return fail(err, NSGCQT_EINVAL, "batch must be >= 1");
     if (sliced && (N % 8) != 0)
         return fail(err, NSGCQT_EINVAL, "slice length must be a multiple of 8");
-    if (N > (int64_t(1) << 30))
-        return fail(err, NSGCQT_EUNSUPPORTED, "n_samples above 2^30");
+    // the band kernels address a signal's packed spectrum and coefficient row
+    // with 32-bit byte offsets
+    if (N >= (int64_t(1) << 29))
+        return fail(err, NSGCQT_EUNSUPPORTED, "n_samples of 2^29 or more");
 
     p.fs = fs; p.fmin = fmin; p.fmax = fmax; p.bpo = B;
     p.N = N; p.L = N / 2; p.batch = batch; p.sliced = sliced;
@@ -481,8 +483,12 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             const int n = work[l];
             // 2^lg interleaved signals: at most 16, within E elements, and no
             // more than the batch needs
+            // and the byte offsets of 2^lg rows of Z and of coefficients below 2^32
             int lg = 4;
-            while (lg > 0 && ((1 << lg) * n > E || (1 << (lg - 1)) >= batch)) --lg;
+            const int64_t row = std::max<int64_t>(p.L + 1, p.C) * 8;
+            while (lg > 0 && ((1 << lg) * n > E || (1 << (lg - 1)) >= batch ||
+                              (int64_t(1) << lg) * row >= (int64_t(1) << 32)))
+                --lg;
             const int G = 1 << lg;
             bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg));
             for (int s0 = 0; s0 < batch; s0 += G)
