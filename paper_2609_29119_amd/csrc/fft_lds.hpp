@@ -249,104 +249,164 @@ __device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb,
     __syncthreads();
 }
 
-// Stockham stage for an odd prime radix R (17 <= R <= kGenericMaxRadix) known
-// only at run time. First each pair of inputs (r, R-r) is twiddled and
-// replaced in place by s_r = y_r + y_{R-r}, d_r = y_r - y_{R-r}; then each
-// work item (butterfly, group of four q) forms the output pairs q, R-q of
-// DftPrime from s, d and the table wr[t] = omega_R^t.
-template <int NT, int EPT>
-__device__ __forceinline__ void stage_generic(float2* buf, int n, int S, int lgnb, int Ns, int R,
-                                              const float2* __restrict__ tws, float2* wr,
-                                              const float2* __restrict__ full) {
-    constexpr int IPT = (EPT + 4) / 5;   // items <= NT EPT (R + 7) / (8 R) <= 0.18 NT EPT
+// First half of a Stockham stage of odd prime radix R: each pair of inputs
+// (r, R - r), r = 1..h, of every butterfly is multiplied by its stage twiddle
+// and replaced in place by s_r = y_r + y_{R-r} (at r) and d_r = y_r - y_{R-r}
+// (at R - r). Input 0 carries no twiddle.
+template <int NT>
+__device__ __forceinline__ void prime_fold(float2* buf, int n, int S, int lgnb, int Ns, int R,
+                                           const float2* __restrict__ tws) {
     const int tid = stage_tid();
+    const int m = n / R;
+    const int h = (R - 1) >> 1;
+    const int nbm = (1 << lgnb) - 1;
+    const int mS = __mul24(m, S);
+    const int totb = m << lgnb;
+    const Div dns = mkdiv(Ns), dh = mkdiv(h);
+    const int total = __mul24(totb, h);
+    // four pairs at a time, all twiddle reads issued first
+    constexpr int U = 4;
+    for (int e0 = tid; e0 < total; e0 += U * NT) {
+        int ia[U], ic[U];
+        float2 wa[U], wc[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            int r1;
+            const int j = qdiv(min(e0 + u * NT, total - 1), dh, r1);
+            const int r = r1 + 1;
+            const int jj = j >> lgnb;
+            const int a0 = __mul24(jj, S) + (j & nbm);
+            ia[u] = a0 + __mul24(r, mS);
+            ic[u] = a0 + __mul24(R - r, mS);
+            wa[u] = make_float2(1.f, 0.f);
+            wc[u] = make_float2(1.f, 0.f);
+            if (Ns > 1) {
+                int k;
+                qdiv(jj, dns, k);
+                const float2* w = tws + __mul24(k, R - 1);
+                wa[u] = w[r - 1];
+                wc[u] = w[R - r - 1];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (e0 + u * NT < total) {
+                const float2 ya = cmul(buf[ia[u]], wa[u]), yc = cmul(buf[ic[u]], wc[u]);
+                buf[ia[u]] = cadd(ya, yc);
+                buf[ic[u]] = csub(ya, yc);
+            }
+        }
+    }
+}
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Stockham stage for an odd prime radix R (17 <= R <= kMfmaMaxRadix) known
+// only at run time, on the matrix cores. After the fold, the outputs of butterfly column c are
+//   X_q     = y_0 + A_q - i B_q,   X_{R-q} = y_0 + A_q + i B_q,   q = 0..h,
+//   A_q = sum_r cos(2 pi q r / R) s_r,   B_q = sum_r sin(2 pi q r / R) d_r,
+// i.e. products of fixed real h x h matrices with the real and imaginary
+// parts of s and d. Real columns come in pairs (re, im) of one butterfly; the
+// sine product reads d with the parts swapped, so the lane of each real part
+// ends up with everything its two outputs need:
+//   re lane: X_q = y0 + A_re + B_im,   X_{R-q} = y0 + A_re - B_im
+//   im lane: X_q = y0 + A_im - B_re,   X_{R-q} = y0 + A_im + B_re.
+// v_mfma_f32_16x16x4f32 operands: A (16 x 4) lane l row l % 16, column l / 16;
+// B (4 x 16) lane l row l / 16, column l % 16; result (16 x 16) lane l, entry v
+// at row 4 (l / 16) + v, column l % 16. Each wave takes result tiles
+// (column block, row block) round-robin and keeps at most kMfmaTilesPerWave of
+// them until every wave has read its inputs; the caller guarantees
+// mfma_tiles(totb, R) <= kMfmaTilesPerWave * NT / 64.
+template <int NT>
+__device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int lgnb, int Ns, int R,
+                                                 const float2* __restrict__ tws, const float* __restrict__ amat) {
+    constexpr int NW = NT / 64;
+    constexpr int TPW = kMfmaTilesPerWave;
+    prime_fold<NT>(buf, n, S, lgnb, Ns, R, tws);
+    __syncthreads();
+    const int tid = stage_tid();
+    const int lane = tid & 63, wave = tid >> 6;
     const int m = n / R;
     const int h = (R - 1) >> 1;
     const int nbm = (1 << lgnb) - 1;
     const int mS = __mul24(m, S), NsS = __mul24(Ns, S);
     const int totb = m << lgnb;
-    const Div dns = mkdiv(Ns), dh = mkdiv(h);
-    for (int t = tid; t < R; t += NT) wr[t] = full[__mul24(t, m)];
-    for (int e = tid; e < __mul24(totb, h); e += NT) {
-        int r1;
-        const int j = qdiv(e, dh, r1);
-        const int r = r1 + 1;
-        const int t = j & nbm, jj = j >> lgnb;
-        const int a0 = __mul24(jj, S) + t;
-        const int ia = a0 + __mul24(r, mS), ic = a0 + __mul24(R - r, mS);
-        float2 ya = buf[ia], yc = buf[ic];
-        if (Ns > 1) {
-            int k;
-            qdiv(jj, dns, k);
-            const float2* w = tws + __mul24(k, R - 1);
-            ya = cmul(ya, w[r - 1]);
-            yc = cmul(yc, w[R - r - 1]);
-        }
-        buf[ia] = cadd(ya, yc);
-        buf[ic] = csub(ya, yc);
-    }
-    __syncthreads();
-    const int ng = (h + 4) >> 2;   // groups of four q over 0..h
-    const int items = __mul24(totb, ng);
-    const Div dng = mkdiv(ng);
-    float2 o[IPT][8];
-    int ob[IPT], oq[IPT];
+    const int Qb = (h + 16) >> 4, Kb = (h + 3) >> 2;
+    const int ntiles = ((totb + 7) >> 3) * Qb;
+    const int kk = lane >> 4, part = lane & 1;
+    float* fb = reinterpret_cast<float*>(buf);
+    f32x4 dc[TPW], ds[TPW];
+    float y0[TPW];
 #pragma unroll
-    for (int b = 0; b < IPT; ++b) {
-        const int it = tid + b * NT;
-        ob[b] = -1;
-        if (it < items) {
-            int g;
-            const int j = qdiv(it, dng, g);
-            const int t = j & nbm, jj = j >> lgnb;
-            const int a0 = __mul24(jj, S) + t;
-            const int q0 = g << 2;
-            const float2 y0 = buf[a0];
-            float2 A[4], B[4];
-            int idx[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                A[u] = y0;
-                B[u] = make_float2(0.f, 0.f);
-                idx[u] = 0;
-            }
-            int ia = a0, ic = a0 + __mul24(R, mS);
-            for (int r = 1; r <= h; ++r) {
-                ia += mS;
-                ic -= mS;
-                const float2 sv = buf[ia], dv = buf[ic];
+    for (int i = 0; i < TPW; ++i) {
+        const int tile = wave + i * NW;            // wave-uniform
+        dc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        ds[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        y0[i] = 0.f;
+        if (tile < ntiles) {
+            const int qb = tile % Qb, cb = tile / Qb;
+            const int c = min((cb << 3) + ((lane & 15) >> 1), totb - 1);
+            const int a0 = __mul24(c >> lgnb, S) + (c & nbm);
+            // s_r.part at input r, d_r.(1 - part) at input R - r (r = 4 kb + kk + 1;
+            // columns past h read inputs that the zero matrix entries cancel)
+            int as = 2 * (a0 + __mul24(kk + 1, mS)) + part;
+            int ad = 2 * (a0 + __mul24(R - kk - 1, mS)) + 1 - part;
+            const int step = 8 * mS;
+            const float* ac = amat + qb * Kb * 128 + lane;
+            // four column blocks at a time: all operand reads are issued before
+            // the products that consume them
+            int kb = 0;
+            for (; kb + 4 <= Kb; kb += 4) {
+                float xa[4], xs[4], sv[4], dv[4];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    idx[u] += q0 + u;
-                    if (idx[u] >= R) idx[u] -= R;
-                    const float2 w = wr[idx[u]];          // (cos, -sin) of 2 pi idx / R
-                    A[u].x += sv.x * w.x;
-                    A[u].y += sv.y * w.x;
-                    B[u].x -= dv.x * w.y;
-                    B[u].y -= dv.y * w.y;
+                    xa[u] = ac[128 * u];
+                    xs[u] = ac[128 * u + 64];
+                    sv[u] = fb[as + u * step];
+                    dv[u] = fb[ad - u * step];
                 }
-            }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                o[b][2 * u] = make_float2(A[u].x + B[u].y, A[u].y - B[u].x);       // X_q
-                o[b][2 * u + 1] = make_float2(A[u].x - B[u].y, A[u].y + B[u].x);   // X_{R-q}
+                for (int u = 0; u < 4; ++u) {
+                    dc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[u], sv[u], dc[i], 0, 0, 0);
+                    ds[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xs[u], dv[u], ds[i], 0, 0, 0);
+                }
+                as += 4 * step;
+                ad -= 4 * step;
+                ac += 512;
             }
-            int k = 0;
-            if (Ns > 1) qdiv(jj, dns, k);
-            ob[b] = __mul24(__mul24(jj - k, R) + k, S) + t;
-            oq[b] = q0;
+            for (; kb < Kb; ++kb) {
+                const float xa = ac[0], xs = ac[64], sv = fb[as], dv = fb[ad];
+                dc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa, sv, dc[i], 0, 0, 0);
+                ds[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xs, dv, ds[i], 0, 0, 0);
+                as += step;
+                ad -= step;
+                ac += 128;
+            }
+            y0[i] = fb[2 * a0 + part];
         }
     }
     __syncthreads();
+    const Div dns = mkdiv(Ns);
 #pragma unroll
-    for (int b = 0; b < IPT; ++b) {
-        if (ob[b] >= 0) {
+    for (int i = 0; i < TPW; ++i) {
+        const int tile = wave + i * NW;
+        if (tile < ntiles) {
+            const int qb = tile % Qb, cb = tile / Qb;
+            const int c = (cb << 3) + ((lane & 15) >> 1);
+            if (c < totb) {
+                const int t = c & nbm, jj = c >> lgnb;
+                int k = 0;
+                if (Ns > 1) qdiv(jj, dns, k);
+                const int ob = 2 * (__mul24(__mul24(jj - k, R) + k, S) + t) + part;
+                const float sg = part ? -1.f : 1.f;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int q = oq[b] + u;
-                if (q <= h) {
-                    buf[ob[b] + __mul24(q, NsS)] = o[b][2 * u];
-                    if (q) buf[ob[b] + __mul24(R - q, NsS)] = o[b][2 * u + 1];
+                for (int v = 0; v < 4; ++v) {
+                    const int q = (qb << 4) + 4 * kk + v;
+                    if (q <= h) {
+                        const float a = y0[i] + dc[i][v], b = sg * ds[i][v];
+                        fb[ob + 2 * __mul24(q, NsS)] = a + b;
+                        if (q) fb[ob + 2 * __mul24(R - q, NsS)] = a - b;
+                    }
                 }
             }
         }
@@ -355,16 +415,16 @@ __device__ __forceinline__ void stage_generic(float2* buf, int n, int S, int lgn
 }
 
 // Forward DFTs of nb = 2^lgnb sequences of length d->n, element i of
-// sequence t at buf[i S + t]. `wr` is LDS scratch for kWrSlots values; the
-// stage twiddles are read from the pool (each butterfly reads R - 1
-// consecutive values, shared by every workgroup of the same length, so they
-// stay in the caches). Ends with a barrier when there is a stage.
+// sequence t at buf[i S + t]. The stage twiddles and prime-radix matrices are
+// read from the pool (each butterfly reads R - 1 consecutive twiddles, shared
+// by every workgroup of the same length, so they stay in the caches). The
+// plan guarantees that every prime-radix stage's result tiles fit the
+// workgroup. Ends with a barrier when there is a stage.
 template <int NT, int EPT>
 __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftDesc* __restrict__ d,
-                                        const float2* __restrict__ pool, float2* wr) {
+                                        const float2* __restrict__ pool) {
     const int n = d->n;
     const int ns = d->nstages;
-    const float2* full = pool + d->full;
     int Ns = 1;
     for (int s = 0; s < ns; ++s) {
         const int R = d->radix[s];
@@ -385,7 +445,9 @@ __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftD
             case 14: stage_fixed<14, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
             case 15: stage_fixed<15, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
             case 16: stage_fixed<16, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            default: stage_generic<NT, EPT>(buf, n, S, lgnb, Ns, R, tw, wr, full); break;
+            default:
+                stage_prime_mfma<NT>(buf, n, S, lgnb, Ns, R, tw, reinterpret_cast<const float*>(pool + d->mat[s]));
+                break;
         }
         Ns *= R;
     }

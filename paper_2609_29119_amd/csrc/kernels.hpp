@@ -17,8 +17,6 @@
 
 namespace nsg {
 
-static_assert(kGenericMaxRadix <= kWrSlots, "generic radix table exceeds its LDS slots");
-
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
 // caps each kernel at 256 VGPRs per lane.
 #define NSG_OCC __attribute__((amdgpu_waves_per_eu(2)))
@@ -97,12 +95,9 @@ __device__ __forceinline__ void load_phase(int total, Get get, Put put) {
     }
 }
 
-// LDS of the pass kernels: generic radix table, four-step twiddles (hi then
-// lo, pass A only), data.
-__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_tw4, float2*& wr, float2*& t4,
-                                         float2*& buf) {
-    wr = lds;
-    t4 = wr + kWrSlots;
+// LDS of the pass kernels: four-step twiddles (hi then lo, pass A only), data.
+__device__ __forceinline__ void pass_lds(float2* lds, const Pass& p, bool with_tw4, float2*& t4, float2*& buf) {
+    t4 = lds;
     buf = t4 + (with_tw4 ? p.nhi4 + (1 << p.split) : 0);
 }
 
@@ -126,8 +121,8 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
                                                       Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
     extern __shared__ float2 lds[];
-    float2 *wr, *t4, *buf;
-    pass_lds(lds, p, true, wr, t4, buf);
+    float2 *t4, *buf;
+    pass_lds(lds, p, true, t4, buf);
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
@@ -172,7 +167,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
             });
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
@@ -206,8 +201,8 @@ template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
                                                       Pass p, Tables T, int batch, long long C) {
     extern __shared__ float2 lds[];
-    float2 *wr, *t4, *buf;
-    pass_lds(lds, p, true, wr, t4, buf);
+    float2 *t4, *buf;
+    pass_lds(lds, p, true, t4, buf);
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
@@ -255,7 +250,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
         }
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
     for (int e = threadIdx.x; e < tot; e += NT) {
@@ -276,8 +271,8 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
                                                        Pass p, Tables T, int batch, long long out_stride,
                                                        float inv_L) {
     extern __shared__ float2 lds[];
-    float2 *wr, *t4, *buf;
-    pass_lds(lds, p, false, wr, t4, buf);
+    float2 *t4, *buf;
+    pass_lds(lds, p, false, t4, buf);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
@@ -297,7 +292,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
             buf[__mul24(n2, S) + r] = r < rows ? v : make_float2(0.f, 0.f);
         });
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
     float2* os = out + (long long)sig * out_stride;
     for (int e = threadIdx.x; e < tot; e += NT) {
         const int r = e & nbm, k2 = e >> p.lgnb;
@@ -361,7 +356,7 @@ __device__ __forceinline__ void blu_middle(float2* buf, int n, int lg, int S, in
 // with w the band's weight at k (g for T, the S^dagger weight for S^dagger),
 // places conj(u) at slot (k - k_c) mod M in LDS, and the band's inverse DFT
 // (eq. 2) is conj(F_M conj(u)) / M. Bands whose length has a prime factor
-// above kGenericMaxRadix use Bluestein's algorithm: with ch_m = exp(-i pi m^2/M),
+// above kMfmaMaxRadix (or for which it is cheaper) use Bluestein's algorithm: with ch_m = exp(-i pi m^2/M),
 // F_M v = ch * conj(F_P conj(F_P(ch v) * K)) where K = F_P(b)/P and b the
 // cyclic chirp exp(+i pi t^2/M), |t| < M.
 template <int NT, int EPT>
@@ -374,8 +369,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
-    float2* wr = lds;
-    float2* buf = wr + kWrSlots;
+    float2* buf = lds;
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
@@ -417,11 +411,11 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
     if (blu) {
         blu_middle<NT>(buf, n, lg, S, sg, T.kern + bd.kern);
         __syncthreads();
-        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
+        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
     }
     if (!live) return;
     float2* cb = coef + (long long)it.s0 * C + bd.off;
@@ -451,8 +445,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
-    float2* wr = lds;
-    float2* buf = wr + kWrSlots;
+    float2* buf = lds;
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
@@ -475,11 +468,11 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __r
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
     if (blu) {
         blu_middle<NT>(buf, n, lg, S, sg, T.kern + bd.kern);
         __syncthreads();
-        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw, wr);
+        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
     }
     if (!live) return;
     const float* w = wt + bd.off;
@@ -535,8 +528,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
     const BandDev bd = T.bands[bg.band];
     const FftDesc* fdn = T.ffts + bg.fftn;
     const FftDesc* fd1 = T.ffts + bg.fft1;
-    float2* wr = lds;
-    float2* t4 = wr + kWrSlots;
+    float2* t4 = lds;
     const int nt4 = fdn->nhi + (1 << fdn->lg);
     float2* buf = t4 + nt4;
     for (int i = threadIdx.x; i < nt4; i += NT) t4[i] = T.tw[fdn->full + fdn->n + i];
@@ -579,7 +571,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
         buf[__mul24(r, S) + c] = v;
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd1, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, lg, fd1, T.tw);
     __syncthreads();
     float2* Y = a.H1 + hbase;
     for (int e = threadIdx.x; e < tot; e += NT) {
@@ -601,8 +593,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int i
     const BigDesc bg = T.bigs[it.big];
     const BandDev bd = T.bands[bg.band];
     const FftDesc* fd2 = T.ffts + bg.fft2;
-    float2* wr = lds;
-    float2* buf = wr + kWrSlots;
+    float2* buf = lds;
     const int M = bd.M;
     const bool blu = bd.chirp >= 0;
     const int lg = bg.lgb, nbm = (1 << lg) - 1, S = seq_stride(lg);
@@ -618,7 +609,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int i
         buf[__mul24(c, S) + r] = r < rows ? Y[e] : make_float2(0.f, 0.f);
     }
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd2, T.tw, wr);
+    lds_fft<NT, EPT>(buf, S, lg, fd2, T.tw);
     const bool to_mid = blu && !second;
     for (int e = threadIdx.x; e < tot; e += NT) {
         const int r = e & nbm, k2 = e >> lg;

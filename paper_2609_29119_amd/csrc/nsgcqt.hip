@@ -149,10 +149,10 @@ Pass pass_b(const HostPlan& h) {
 }
 
 int lds_pass_a(const Pass& q) {
-    return (kWrSlots + q.nhi4 + (1 << q.split) + lds_slots(q.L1, q.lgnb)) * static_cast<int>(sizeof(float2));
+    return (q.nhi4 + (1 << q.split) + lds_slots(q.L1, q.lgnb)) * static_cast<int>(sizeof(float2));
 }
 int lds_pass_b(const Pass& q) {
-    return (kWrSlots + lds_slots(q.L2, q.lgnb)) * static_cast<int>(sizeof(float2));
+    return lds_slots(q.L2, q.lgnb) * static_cast<int>(sizeof(float2));
 }
 
 #define DISPATCH_NT(nt, KERNEL, ...)                                                         \
@@ -214,7 +214,7 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
               hipStream_t s) {
     const HostPlan& h = p->h;
     for (const auto& bk : h.buckets) {
-        const int lds = (kWrSlots + bk.lds_elems) * static_cast<int>(sizeof(float2));
+        const int lds = bk.lds_elems * static_cast<int>(sizeof(float2));
         const dim3 grid(bk.nitems), block(bk.nt);
         auto go = [&](auto ka, auto ks) -> int {
             if (analysis) {

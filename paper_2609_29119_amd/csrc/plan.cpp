@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <complex>
+#include <limits>
 #include <map>
 
 #include "../../include/nsgcqt.h"
@@ -69,7 +70,7 @@ void push_c(std::vector<float>& v, cd z) {
 
 }  // namespace
 
-bool factor_radices(int64_t n, std::vector<int>& out) {
+bool factor_radices(int64_t n, std::vector<int>& out, int max_prime) {
     out.clear();
     if (n < 1) return false;
     // prime factors, largest first
@@ -79,12 +80,13 @@ bool factor_radices(int64_t n, std::vector<int>& out) {
         while (m % p == 0) { f.push_back(p); m /= p; }
     if (m > 1) f.push_back(m);
     std::sort(f.rbegin(), f.rend());
-    // primes above 16 are stages of their own (generic radix, up to 61);
-    // the rest are packed greedily into compile-time radices of at most 16
+    // primes above 16 are stages of their own (runtime radix, up to
+    // max_prime); the rest are packed greedily into compile-time radices of
+    // at most 16
     std::vector<int64_t> small;
     for (int64_t p : f) {
         if (p > 16) {
-            if (p > kGenericMaxRadix) return false;
+            if (p > max_prime) return false;
             out.push_back(static_cast<int>(p));
         } else {
             small.push_back(p);
@@ -111,7 +113,31 @@ namespace {
 struct FftRegistry {
     HostPlan& p;
     std::map<int64_t, int> index;
+    std::map<int, int32_t> mats;   // prime radix -> offset of its matrix fragments
     explicit FftRegistry(HostPlan& plan) : p(plan) {}
+
+    // Matrix-core fragments of the cosine and sine matrices of prime R (layout
+    // in FftDesc::mat), angles reduced exactly: (q r) mod R.
+    int32_t matrix(int R) {
+        auto it = mats.find(R);
+        if (it != mats.end()) return it->second;
+        const int h = (R - 1) / 2, Qb = (h + 16) >> 4, Kb = (h + 3) >> 2;
+        const int32_t off = static_cast<int32_t>(p.twpool.size() / 2);
+        for (int qb = 0; qb < Qb; ++qb)
+            for (int kb = 0; kb < Kb; ++kb)
+                for (int which = 0; which < 2; ++which)
+                    for (int l = 0; l < 64; ++l) {
+                        const int q = 16 * qb + l % 16, r = 4 * kb + l / 16 + 1;
+                        double v = 0.0;
+                        if (q <= h && r <= h) {
+                            const double ang = 2.0 * kPi * static_cast<double>((q * r) % R) / R;
+                            v = which ? std::sin(ang) : std::cos(ang);
+                        }
+                        p.twpool.push_back(static_cast<float>(v));
+                    }
+        mats[R] = off;
+        return off;
+    }
 
     // Index of the FftDesc for length n, creating it (and its twiddles) on
     // first use; -1 if n does not factor into supported radices.
@@ -123,10 +149,9 @@ struct FftRegistry {
         FftDesc d{};
         d.n = static_cast<int32_t>(n);
         d.nstages = static_cast<int32_t>(rad.size());
-        d.max_generic = 0;
         for (size_t s = 0; s < rad.size(); ++s) {
             d.radix[s] = static_cast<int16_t>(rad[s]);
-            if (rad[s] > 16) d.max_generic = std::max(d.max_generic, rad[s]);
+            d.mat[s] = rad[s] > 16 ? matrix(rad[s]) : -1;
         }
         d.full = static_cast<int32_t>(p.twpool.size() / 2);
         for (int64_t t = 0; t < n; ++t) push_c(p.twpool, root(t, n));
@@ -161,6 +186,84 @@ struct FftRegistry {
 int fail(std::string& err, int code, const std::string& msg) {
     err = msg;
     return code;
+}
+
+// Band kernel tiers by transform length: threads and elements per thread.
+struct Tier { int max_work, nt, ept; };
+constexpr Tier kTiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}};
+constexpr int kNumTiers = static_cast<int>(sizeof(kTiers) / sizeof(kTiers[0]));
+
+int tier_of(int64_t n) {
+    for (int i = 0; i < kNumTiers; ++i)
+        if (n <= kTiers[i].max_work) return i;
+    return -1;
+}
+
+// log2 of the interleaved sequences per band work item of a length-n
+// transform: at most 16, within E elements, no more than the batch needs, and
+// 2^lg rows of Z and of coefficients (row_bytes each) within 32-bit offsets.
+int seq_lg(int64_t n, int E, int batch, int64_t row_bytes) {
+    int lg = 4;
+    while (lg > 0 && ((int64_t(1) << lg) * n > E || (1 << (lg - 1)) >= batch ||
+                      (int64_t(1) << lg) * row_bytes >= (int64_t(1) << 32)))
+        --lg;
+    return lg;
+}
+
+// True when every prime-radix stage (R > 16) of a length-n transform keeps
+// its matrix-core result tiles within the workgroup when 2^lg sequences share
+// a workgroup of nt threads.
+bool mfma_fits(const std::vector<int>& rad, int64_t n, int lg, int nt) {
+    for (int R : rad)
+        if (R > 16 && mfma_tiles(static_cast<int>((n / R) << lg), R) > kMfmaTilesPerWave * (nt / 64)) return false;
+    return true;
+}
+
+// Estimated cost, in SIMD cycles per sequence, of a length-n transform with
+// the given radices when 2^lg sequences share a workgroup: about 20 vector
+// instructions per point for a compile-time stage; a matrix-core stage costs
+// its fold and write passes plus 2 Kb products of 32 cycles per result tile.
+double stage_cost(const std::vector<int>& rad, int64_t n, int lg) {
+    double c = 0.0;
+    for (int R : rad) {
+        if (R <= 16) {
+            c += 1.25 * static_cast<double>(n);
+        } else {
+            const int Kb = ((R - 1) / 2 + 3) >> 2;
+            const int tiles = mfma_tiles(static_cast<int>((n / R) << lg), R);
+            c += 0.9 * static_cast<double>(n) + tiles * Kb * 64.0 / static_cast<double>(1 << lg);
+        }
+    }
+    return c;
+}
+
+// Column length n1 of the four-step split n = n1 n2 (n1 <= n2 <= 4096, both
+// with a radix plan) used for transforms beyond the largest tier; -1 if none.
+int64_t huge_split(int64_t n) {
+    int64_t n1 = -1;
+    for (int64_t d = 2; d * d <= n; ++d) {
+        std::vector<int> r1, r2;
+        if (n % d == 0 && n / d <= 4096 && factor_radices(d, r1) && factor_radices(n / d, r2)) n1 = d;
+    }
+    return n1;
+}
+
+// Cost of a length-n band transform in its tier, or, above the largest tier,
+// in the four-step huge-band path; infinite when it cannot run. The choice
+// uses the tier's largest interleave (seq_lg for an unbounded batch), so it
+// and hence every result bit do not depend on the batch size.
+double band_fft_cost(int64_t n, int64_t row_bytes) {
+    std::vector<int> rad;
+    if (!factor_radices(n, rad)) return std::numeric_limits<double>::infinity();
+    const int ti = tier_of(n);
+    if (ti < 0) {
+        if (huge_split(n) < 0) return std::numeric_limits<double>::infinity();
+        return 2.5 * static_cast<double>(n) * static_cast<double>(rad.size());
+    }
+    const Tier& t = kTiers[ti];
+    const int lg = seq_lg(n, t.nt * t.ept, 1 << 30, row_bytes);
+    if (!mfma_fits(rad, n, lg, t.nt)) return std::numeric_limits<double>::infinity();
+    return stage_cost(rad, n, lg);
 }
 
 }  // namespace
@@ -330,7 +433,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         if (best < 0)
             return fail(err, NSGCQT_EUNSUPPORTED,
                         "packed length L = " + std::to_string(L) + " has a prime factor above " +
-                            std::to_string(kGenericMaxRadix));
+                            std::to_string(kMfmaMaxRadix));
         auto& f = p.fs4;
         f.L1 = best; f.L2 = L / best;
         if (f.L2 > 8192) return fail(err, NSGCQT_EUNSUPPORTED, "packed length too large for the two-pass FFT");
@@ -349,12 +452,22 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         pick(f.L2, f.L1, f.tile_b, f.nt_b);
         if ((int64_t(1) << f.tile_a) * f.L1 > 8192 || (int64_t(1) << f.tile_b) * f.L2 > 8192)
             return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds one workgroup");
+        // fewer columns per workgroup until the prime stages' matrix tiles fit
+        {
+            std::vector<int> r1, r2;
+            factor_radices(f.L1, r1);
+            factor_radices(f.L2, r2);
+            while (f.tile_a > 0 && !mfma_fits(r1, f.L1, f.tile_a, f.nt_a)) --f.tile_a;
+            while (f.tile_b > 0 && !mfma_fits(r2, f.L2, f.tile_b, f.nt_b)) --f.tile_b;
+            if (!mfma_fits(r1, f.L1, f.tile_a, f.nt_a) || !mfma_fits(r2, f.L2, f.tile_b, f.nt_b))
+                return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass: prime stage exceeds the workgroup");
+        }
         {
             int lg4 = 0;
             while ((int64_t(1) << (2 * lg4)) < L) ++lg4;
             const int64_t t4 = ((L + (int64_t(1) << lg4) - 1) >> lg4) + (int64_t(1) << lg4);
-            const int64_t a_slots = kWrSlots + t4 + lds_slots(static_cast<int>(f.L1), f.tile_a);
-            const int64_t b_slots = kWrSlots + lds_slots(static_cast<int>(f.L2), f.tile_b);
+            const int64_t a_slots = t4 + lds_slots(static_cast<int>(f.L1), f.tile_a);
+            const int64_t b_slots = lds_slots(static_cast<int>(f.L2), f.tile_b);
             if (a_slots * 8 > 160 * 1024 || b_slots * 8 > 160 * 1024)
                 return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds LDS");
         }
@@ -369,6 +482,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
 
     // ---- band transforms: mixed radix, or Bluestein over a 7-smooth length
     p.banddev.clear(); p.chirp.clear(); p.kern.clear();
+    const int64_t row_bytes = std::max<int64_t>(p.L + 1, p.C) * 8;
     std::vector<int> work(p.bands.size());
     for (size_t l = 0; l < p.bands.size(); ++l) {
         const auto& b = p.bands[l];
@@ -379,13 +493,17 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         d.off = static_cast<int32_t>(b.off);
         d.inv_M = static_cast<float>(1.0 / static_cast<double>(b.M));
         d.chirp = -1; d.kern = -1;
-        int id = reg.get(b.M);
-        if (id >= 0) {
-            d.fft = id;
-            work[l] = static_cast<int>(b.M);
+        // direct transform of length M, or Bluestein over P, whichever the
+        // cost model prefers
+        const int64_t M = b.M;
+        const int64_t P = smooth7_at_least(2 * M - 1);
+        const double c_direct = band_fft_cost(M, row_bytes);
+        const double c_blu = 2.0 * band_fft_cost(P, row_bytes) + 0.6 * static_cast<double>(P);
+        if (c_direct <= c_blu) {
+            d.fft = reg.get(M);
+            if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no radix plan for a band");
+            work[l] = static_cast<int>(M);
         } else {
-            const int64_t M = b.M;
-            const int64_t P = smooth7_at_least(2 * M - 1);
             d.fft = reg.get(P);
             if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no Bluestein length");
             d.chirp = static_cast<int32_t>(p.chirp.size() / 2);
@@ -413,10 +531,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     }
 
     // ---- buckets by transform length
-    struct Tier { int max_work, nt, ept; };
-    const Tier tiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}};
     p.buckets.clear();
-    for (const auto& t : tiers) {
+    for (const auto& t : kTiers) {
         Bucket bk{};
         bk.nt = t.nt; bk.ept = t.ept; bk.max_work = 0; bk.coeffs = 0;
         p.buckets.push_back(bk);
@@ -424,17 +540,11 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     p.bigs.clear(); p.bigitems.clear(); p.Hn = 0; p.C_big = 0; p.Hn_blu = 0; p.C_big_blu = 0;
     int big_t4 = 0, big_ea = 0, big_eb = 0;
     for (size_t l = 0; l < p.bands.size(); ++l) {
-        int ti = -1;
-        for (int i = 0; i < 4; ++i)
-            if (work[l] <= tiers[i].max_work) { ti = i; break; }
+        const int ti = tier_of(work[l]);
         if (ti < 0) {
             // four-step through global memory: n = n1 n2, n1 <= n2 <= 4096
             const int64_t n = work[l];
-            int64_t n1 = -1;
-            for (int64_t d = 2; d * d <= n; ++d) {
-                std::vector<int> r1, r2;
-                if (n % d == 0 && n / d <= 4096 && factor_radices(d, r1) && factor_radices(n / d, r2)) n1 = d;
-            }
+            const int64_t n1 = huge_split(n);
             if (n1 < 0)
                 return fail(err, NSGCQT_EUNSUPPORTED,
                             "band of length " + std::to_string(p.bands[l].M) + " needs a transform of " +
@@ -449,10 +559,21 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             g.fft2 = reg.get(g.n2);
             if (g.fftn < 0 || g.fft1 < 0 || g.fft2 < 0)
                 return fail(err, NSGCQT_EUNSUPPORTED, "huge band transform has no radix plan");
+            // columns / rows per workgroup of 512 threads: at most 16, within
+            // 4096 elements, and with the prime stages' matrix tiles fitting
+            std::vector<int> r1, r2;
+            factor_radices(g.n1, r1);
+            factor_radices(g.n2, r2);
             g.lga = 4;
-            while (g.lga > 0 && ((1 << g.lga) * g.n1 > 4096 || (1 << (g.lga - 1)) >= g.n2)) --g.lga;
+            while (g.lga > 0 && ((1 << g.lga) * g.n1 > 4096 || (1 << (g.lga - 1)) >= g.n2 ||
+                                 !mfma_fits(r1, g.n1, g.lga, 512)))
+                --g.lga;
             g.lgb = 4;
-            while (g.lgb > 0 && ((1 << g.lgb) * g.n2 > 4096 || (1 << (g.lgb - 1)) >= g.n1)) --g.lgb;
+            while (g.lgb > 0 && ((1 << g.lgb) * g.n2 > 4096 || (1 << (g.lgb - 1)) >= g.n1 ||
+                                 !mfma_fits(r2, g.n2, g.lgb, 512)))
+                --g.lgb;
+            if (!mfma_fits(r1, g.n1, g.lga, 512) || !mfma_fits(r2, g.n2, g.lgb, 512))
+                return fail(err, NSGCQT_EUNSUPPORTED, "huge band: prime stage exceeds the workgroup");
             g.hoff = static_cast<int32_t>(p.Hn);
             p.Hn += n;
             p.C_big += p.bands[l].M;
@@ -481,21 +602,15 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         bk.lds_elems = 0;
         for (int32_t l : bk.bands) {
             const int n = work[l];
-            // 2^lg interleaved signals: at most 16, within E elements, and no
-            // more than the batch needs
-            // and the byte offsets of 2^lg rows of Z and of coefficients below 2^32
-            int lg = 4;
-            const int64_t row = std::max<int64_t>(p.L + 1, p.C) * 8;
-            while (lg > 0 && ((1 << lg) * n > E || (1 << (lg - 1)) >= batch ||
-                              (int64_t(1) << lg) * row >= (int64_t(1) << 32)))
-                --lg;
+            // 2^lg interleaved signals (seq_lg, as in the cost model)
+            const int lg = seq_lg(n, E, batch, row_bytes);
             const int G = 1 << lg;
             bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg));
             for (int s0 = 0; s0 < batch; s0 += G)
                 p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), lg});
         }
         bk.nitems = static_cast<int>(p.items.size()) - bk.item_off;
-        if ((kWrSlots + bk.lds_elems) * 8 > 160 * 1024)
+        if (bk.lds_elems * 8 > 160 * 1024)
             return fail(err, NSGCQT_EUNSUPPORTED, "band kernel exceeds LDS");
     }
 
@@ -512,8 +627,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         }
         p.big_n[pass] = static_cast<int>(p.bigitems.size()) - p.big_off[pass];
     }
-    p.big_lds_a = static_cast<int>((kWrSlots + big_t4 + big_ea) * 8);
-    p.big_lds_b = static_cast<int>((kWrSlots + big_eb) * 8);
+    p.big_lds_a = static_cast<int>((big_t4 + big_ea) * 8);
+    p.big_lds_b = static_cast<int>(big_eb * 8);
     if (!p.bigs.empty() && (p.big_lds_a > 160 * 1024 || p.big_lds_b > 160 * 1024))
         return fail(err, NSGCQT_EUNSUPPORTED, "huge-band pass exceeds LDS");
 

@@ -91,8 +91,10 @@ struct HostPlan {
 int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int bpo,
                     int64_t N, int batch, bool sliced, std::string& err);
 
-// Radix factorisation used by the Stockham stages: true when n factors into
-// 2, 3, 4, 5, 7, 8 and primes up to kGenericMaxRadix.
-bool factor_radices(int64_t n, std::vector<int>& radices);
+// Radix factorisation used by the Stockham stages: primes above 16 (at most
+// max_prime) become stages of their own, the remaining factors are packed
+// greedily into radices of at most 16. False when n has a larger prime factor
+// or needs more than kMaxStages stages.
+bool factor_radices(int64_t n, std::vector<int>& radices, int max_prime = kMfmaMaxRadix);
 
 }  // namespace nsg

@@ -6,11 +6,21 @@
 
 namespace nsg {
 
-// Largest prime handled by the direct odd-radix Stockham stage. Lengths with a
-// larger prime factor are transformed with Bluestein's chirp-z algorithm over a
-// 7-smooth length P >= 2M - 1.
-constexpr int kGenericMaxRadix = 61;
+// Largest prime radix of a Stockham stage. Primes above 16 run on the matrix
+// cores, which form the stage's outputs as products with the cosine and sine
+// matrices of the prime. Band lengths with a larger prime factor, or whose
+// stage does not fit a workgroup's matrix tiles, are transformed with
+// Bluestein's chirp-z algorithm over a 7-smooth length P >= 2M - 1, which is
+// also used where the cost model finds it cheaper.
+constexpr int kMfmaMaxRadix = 257;
 constexpr int kMaxStages = 24;
+// 16 x 16 result tiles one wave keeps in registers across the barrier of a
+// matrix-core stage.
+constexpr int kMfmaTilesPerWave = 4;
+
+// Result tiles of a matrix-core stage of prime radix R over totb butterfly
+// columns: blocks of 8 complex columns times blocks of 16 outputs q = 0..(R-1)/2.
+inline constexpr int mfma_tiles(int totb, int R) { return ((totb + 7) >> 3) * (((R - 1) / 2 + 16) >> 4); }
 
 // One transform length n: Stockham stages of the given radices, applied in
 // order. Twiddle pool layout per length: the full table omega_n^t (t < n) at
@@ -26,13 +36,17 @@ struct FftDesc {
     int32_t nhi;
     int32_t stw;
     int32_t ntw;
-    int32_t max_generic;     // largest runtime (odd prime > 16) radix, 0 if none
     int16_t radix[kMaxStages];
     int32_t stoff[kMaxStages];
+    // per stage with a prime radix R > 16: pool offset (in complex entries) of
+    // the matrix-core fragments of cos(2 pi q r / R) and sin(2 pi q r / R),
+    // rows q = 0..h, columns r = 1..h (h = (R - 1) / 2), zero-padded to
+    // Qb = (h + 16) / 16 row blocks of 16 and Kb = (h + 3) / 4 column blocks of
+    // 4; fragment (qb, kb, which) holds 64 floats at ((qb Kb + kb) 2 + which)
+    // 64, lane l holding row 16 qb + l % 16 and column 4 kb + l / 16. -1 for
+    // other stages.
+    int32_t mat[kMaxStages];
 };
-
-// LDS slots reserved for the table of a generic odd-prime radix.
-constexpr int kWrSlots = 64;
 
 // One band of the layout as the band kernels see it.
 struct BandDev {

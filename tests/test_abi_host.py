@@ -178,9 +178,12 @@ def test_empty_bands_dropped_identically(lib):
 
 
 def test_unsupported_packed_length(lib):
-    # L = 2 * 67 has a prime factor above the largest packed-FFT radix
-    st, _ = _status(lib.nsgcqt_plan_create_host, 268.0, 4.0, 134.0, 4, 268, 1)
+    # L = 2 * 263 has a prime factor above the largest Stockham radix (257)
+    st, _ = _status(lib.nsgcqt_plan_create_host, 1052.0, 4.0, 526.0, 4, 1052, 1)
     assert st == nb.EUNSUPPORTED
+    # L = 2 * 67 runs its prime factor as a matrix-core stage
+    st, _ = _status(lib.nsgcqt_plan_create_host, 268.0, 4.0, 134.0, 4, 268, 1)
+    assert st == nb.OK
 
 
 def test_sliced_plan_rules(lib):

@@ -39,9 +39,12 @@ def to_np(t):
 
 
 # (name, fs, fmin, fmax, bins/oct, N, batch): small layouts spanning several
-# tiles, ragged tails, odd packed lengths, generic radices and Bluestein bands
+# tiles, ragged tails, odd packed lengths, prime-radix (matrix-core) stages in
+# the bands and in the packed FFT (L = 2 * 67, 2 * 257), and Bluestein bands
 SMALL = [
     ("N500_L250", 250.0, 4.0, 125.0, 4, 500, 2),
+    ("N268_L2x67", 268.0, 4.0, 134.0, 4, 268, 2),
+    ("N1028_L2x257", 1028.0, 8.0, 514.0, 6, 1028, 3),
     ("N250_oddL", 250.0, 4.0, 125.0, 3, 250, 1),
     ("N4620_radix11", 4620.0, 30.0, 2310.0, 12, 4620, 3),
     ("N6000_b5", 8000.0, 50.0, 4000.0, 24, 6000, 5),
