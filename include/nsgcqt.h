@@ -192,11 +192,12 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan plan, const float* coeffs, int64_t n, f
                              void* ws, size_t ws_bytes, void* stream);
 
 /* Profiling hook. While `events` is non-NULL, every compute call on this
- * plan records events[0] on its stream before its first kernel and
- * events[i+1] after its i-th kernel, for as many events as given
- * (hipEvent_t handles created by the caller). NULL stops recording. The
- * setting is plan state: do not combine it with concurrent calls on the
- * same plan. */
+ * plan brackets its i-th kernel launch with events[2i] (before) and
+ * events[2i+1] (after), both recorded on the call's stream, for as many
+ * pairs as given (hipEvent_t handles created by the caller; NULL entries
+ * are skipped, so single kernels can be timed alone). The kernel order is
+ * that of nsgcqt_stage_info. A NULL `events` stops recording. The setting
+ * is plan state: do not combine it with concurrent calls on the same plan. */
 int nsgcqt_set_stage_events(nsgcqt_plan plan, void* const* events, int n_events);
 
 /* Kernels one call of `op` enqueues (non-sliced plans): returns their

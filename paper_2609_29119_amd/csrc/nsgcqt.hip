@@ -2,6 +2,7 @@
 // fp64, uploaded once as fp32), and the enqueue-only compute calls.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -113,6 +114,15 @@ int upload(nsgcqt_plan_s* p) {
     return NSGCQT_OK;
 }
 
+// Releases the plan's device tables.
+int release(nsgcqt_plan_s* p) {
+    if (!p->dmem) return NSGCQT_OK;
+    const hipError_t e = hipFree(p->dmem);
+    p->dmem = nullptr;
+    if (e != hipSuccess) return set_err(NSGCQT_EDEVICE, std::string("hipFree: ") + hipGetErrorString(e));
+    return NSGCQT_OK;
+}
+
 // ---------------------------------------------------------------- launches
 template <typename K>
 int launch_prep(K kernel, int lds_bytes) {
@@ -122,8 +132,17 @@ int launch_prep(K kernel, int lds_bytes) {
     return NSGCQT_OK;
 }
 
-void record(nsgcqt_plan_s* p, hipStream_t s) {
-    if (p->ev_next < static_cast<int>(p->events.size())) hipEventRecord(p->events[p->ev_next++], s);
+// Stage timing: with events installed, kernel launch i is bracketed by
+// events[2i] and events[2i + 1] on its stream; NULL entries are skipped.
+void ev_start(nsgcqt_plan_s* p, hipStream_t s) {
+    if (p->ev_next + 1 < static_cast<int>(p->events.size()) && p->events[p->ev_next])
+        hipEventRecord(p->events[p->ev_next], s);
+}
+void ev_end(nsgcqt_plan_s* p, hipStream_t s) {
+    if (p->ev_next + 1 < static_cast<int>(p->events.size())) {
+        if (p->events[p->ev_next + 1]) hipEventRecord(p->events[p->ev_next + 1], s);
+        p->ev_next += 2;
+    }
 }
 
 Pass pass_a(const HostPlan& h) {
@@ -168,10 +187,11 @@ int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl
     const int lds = lds_pass_a(q);
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
+        ev_start(p, s);
         hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch,
                            sig_stride);
         HIP_TRY(hipGetLastError());
-        record(p, s);
+        ev_end(p, s);
         return NSGCQT_OK;
     };
     DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a)
@@ -183,10 +203,11 @@ int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream
     const int lds = lds_pass_a(q);
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
+        ev_start(p, s);
         hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, W, Y, q, p->T, batch,
                            static_cast<long long>(p->h.C));
         HIP_TRY(hipGetLastError());
-        record(p, s);
+        ev_end(p, s);
         return NSGCQT_OK;
     };
     DISPATCH_NT(p->h.fs4.nt_a, k_inv_a)
@@ -200,16 +221,18 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
     const float inv_L = static_cast<float>(1.0 / static_cast<double>(p->h.L));
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
+        ev_start(p, s);
         hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_b), lds, s, Y, out, q, p->T, batch,
                            out_stride, inv_L);
         HIP_TRY(hipGetLastError());
-        record(p, s);
+        ev_end(p, s);
         return NSGCQT_OK;
     };
     DISPATCH_NT(p->h.fs4.nt_b, k_pass_b, , INV)
     return NSGCQT_OK;
 }
 
+// The band tiers, one launch each.
 int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float* wt, int batch,
               hipStream_t s) {
     const HostPlan& h = p->h;
@@ -217,6 +240,7 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
         const int lds = bk.lds_elems * static_cast<int>(sizeof(float2));
         const dim3 grid(bk.nitems), block(bk.nt);
         auto go = [&](auto ka, auto ks) -> int {
+            ev_start(p, s);
             if (analysis) {
                 if (int r = launch_prep(ka, lds)) return r;
                 hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
@@ -227,15 +251,14 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
                                    static_cast<long long>(h.C));
             }
             HIP_TRY(hipGetLastError());
-            record(p, s);
+            ev_end(p, s);
             return NSGCQT_OK;
         };
         int r = NSGCQT_OK;
         if (bk.nt == 64) r = go(k_band_analysis<64, 8>, k_band_synthesis<64, 8>);
         else if (bk.nt == 256 && bk.ept == 8) r = go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
         else if (bk.nt == 256) r = go(k_band_analysis<256, 16>, k_band_synthesis<256, 16>);
-        else if (bk.nt == 512) r = go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
-        else r = go(k_band_analysis<1024, 16>, k_band_synthesis<1024, 16>);
+        else r = go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
         if (r) return r;
     }
     return NSGCQT_OK;
@@ -254,6 +277,7 @@ int run_big(nsgcqt_plan_s* p, BigArgs a, int batch, hipStream_t s) {
     for (int pass = 0; pass < 4; ++pass) {
         const int n = h.big_n[pass];
         if (n == 0) continue;
+        ev_start(p, s);
         if (pass % 2 == 0)
             hipLaunchKernelGGL(ka, dim3(n), dim3(512), h.big_lds_a, s, a, p->T, h.big_off[pass], n, batch,
                                pass == 0 ? in0 : kBigInBlu2);
@@ -261,7 +285,7 @@ int run_big(nsgcqt_plan_s* p, BigArgs a, int batch, hipStream_t s) {
             hipLaunchKernelGGL(kb, dim3(n), dim3(512), h.big_lds_b, s, a, p->T, h.big_off[pass], n, batch,
                                pass == 3 ? 1 : 0);
         HIP_TRY(hipGetLastError());
-        record(p, s);
+        ev_end(p, s);
     }
     return NSGCQT_OK;
 }
@@ -348,9 +372,10 @@ int create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64
     if (device) {
         r = upload(p);
         if (r != NSGCQT_OK) {
-            if (p->dmem) hipFree(p->dmem);
+            const std::string msg = g_err;
+            release(p);
             delete p;
-            return r;
+            return set_err(r, msg);
         }
     }
     *out = p;
@@ -382,11 +407,7 @@ int nsgcqt_sliced_plan_create_host(nsgcqt_plan* out, double fs, double fmin, dou
 
 int nsgcqt_plan_destroy(nsgcqt_plan p) {
     if (!p) return NSGCQT_OK;
-    int r = NSGCQT_OK;
-    if (p->dmem) {
-        hipError_t e = hipFree(p->dmem);
-        if (e != hipSuccess) r = set_err(NSGCQT_EDEVICE, std::string("hipFree: ") + hipGetErrorString(e));
-    }
+    const int r = release(p);
     delete p;
     return r;
 }
@@ -448,7 +469,6 @@ int nsgcqt_plan_weights(nsgcqt_plan p, int which, float* dst, size_t bytes) {
 int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_t ws_bytes, void* stream) {
     if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, false)) return r;
     p->ev_next = 0;
-    record(p, static_cast<hipStream_t>(stream));
     return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->wA, p->h.batch, SliceIn{0, 0, 0, 0},
                          static_cast<char*>(ws), static_cast<hipStream_t>(stream));
 }
@@ -456,7 +476,6 @@ int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_
 int nsgcqt_synthesise(nsgcqt_plan p, const float* coeffs, float* xo, void* ws, size_t ws_bytes, void* stream) {
     if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, false)) return r;
     p->ev_next = 0;
-    record(p, static_cast<hipStream_t>(stream));
     return chain_synthesise(p, reinterpret_cast<const float2*>(coeffs), xo, p->wS, p->h.batch,
                             static_cast<char*>(ws), static_cast<hipStream_t>(stream));
 }
@@ -468,7 +487,6 @@ int nsgcqt_adjoint(nsgcqt_plan p, int op, const float* in, float* out, void* ws,
     if (int r = check_call(p, in, out, ws, ws_bytes, p ? (ta ? p->h.ws_syn : p->h.ws_an) : 0, false)) return r;
     p->ev_next = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    record(p, s);
     if (ta)
         return chain_synthesise(p, reinterpret_cast<const float2*>(in), out, p->wT, p->h.batch,
                                 static_cast<char*>(ws), s);
@@ -491,7 +509,6 @@ int nsgcqt_sliced_analyse(nsgcqt_plan p, const float* x, int64_t n, float* coeff
     const int64_t J = nsgcqt_sliced_count(p, n);
     hipStream_t s = static_cast<hipStream_t>(stream);
     p->ev_next = 0;
-    record(p, s);
     for (int64_t s0 = 0; s0 < J; s0 += h.spc) {
         const int cnt = static_cast<int>(std::min<int64_t>(h.spc, J - s0));
         SliceIn sl{1, static_cast<int>(s0), static_cast<long long>(n), static_cast<int>(h.N / 2)};
@@ -515,7 +532,6 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, floa
                        reinterpret_cast<float*>(w + chain_bytes + align256(4 * h.N * h.spc) + align256(4 * H))};
     hipStream_t s = static_cast<hipStream_t>(stream);
     p->ev_next = 0;
-    record(p, s);
     int flip = 0;
     for (int64_t s0 = 0; s0 < J; s0 += h.spc) {
         const int cnt = static_cast<int>(std::min<int64_t>(h.spc, J - s0));
@@ -523,10 +539,11 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, floa
         if (int r = chain_synthesise(p, c, y, p->wS, cnt, w, s)) return r;
         const int64_t span = static_cast<int64_t>(cnt) * H;
         const int blocks = static_cast<int>(std::min<int64_t>((span + 255) / 256, 8192));
+        ev_start(p, s);
         hipLaunchKernelGGL(k_ola, dim3(blocks), dim3(256), 0, s, y, carry[flip], carry[flip ^ 1], xo,
                            static_cast<int>(s0), cnt, static_cast<int>(h.N), static_cast<long long>(n));
         HIP_TRY(hipGetLastError());
-        record(p, s);
+        ev_end(p, s);
         flip ^= 1;
     }
     return NSGCQT_OK;

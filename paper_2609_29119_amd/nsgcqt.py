@@ -207,7 +207,8 @@ class Plan:
         return out
 
     def set_stage_events(self, handles):
-        """Record HIP events between kernels (see nsgcqt_set_stage_events); None stops."""
+        """Bracket kernel i of each call with handles[2i], handles[2i+1]
+        (see nsgcqt_set_stage_events); None stops."""
         if not handles:
             _check(lib().nsgcqt_set_stage_events(self._h, None, 0))
             return
