@@ -192,11 +192,25 @@ __device__ __forceinline__ float2 gather_bin(const float2* __restrict__ Ws, int4
 }
 
 // ------------------------------- inverse packed FFT, pass A, with overlap-add
-// For q = n1 L2 + n2 over a tile of columns: X_q and X_{L-q} are summed from
-// the bands that own those bins (no atomics: every packed bin is produced by
-// exactly one thread), made real at DC and Nyquist, and retangled into
-// Z_q = (1/2)[(1 + i conj(w_q)) X_q + (1 - i conj(w_q)) conj(X_{L-q})] (eq. 9).
-// The inverse DFT is taken as conj(F_L conj(Z)) / L.
+// X_q for the packed bins of a tile is summed from the bands that cover the
+// bin (no atomics: every packed bin is produced by exactly one thread), made
+// real at DC and Nyquist, and retangled into
+//   Z_q = (1/2)[(1 + i conj(w_q)) X_q + (1 - i conj(w_q)) conj(X_{L-q})]   (eq. 9).
+// Bins pair up with their mirrors: for q = n1 L2 + n2 with 0 < n2 < L2,
+// L - q = (L1 - 1 - n1) L2 + (L2 - n2). A tile holds H = 2^lgnb / 2 primary
+// columns n2 in [0, L2/2] in slots 0..H-1 and their mirror columns L2 - n2
+// in slots H..2H-1, so one thread gathers X_q and X_{L-q} once and emits both
+// Z_q and Z_{L-q}. Columns equal to their mirror (0, and L2/2 for even L2)
+// pair within the column and leave the mirror slot unused. With a single
+// column per tile (lgnb = 0) tiles are plain columns. The inverse DFT is
+// taken as conj(F_L conj(Z)) / L.
+__device__ __forceinline__ float2 retangle_conj(float2 om, float2 xq, float2 xm) {
+    const float2 pa = make_float2(1.f + om.y, om.x);      // 1 + i conj(w), om = (cos, -sin)
+    const float2 pb = make_float2(1.f - om.y, -om.x);     // 1 - i conj(w)
+    const float2 z = cadd(cmul(pa, xq), cmul(pb, conjf2(xm)));
+    return make_float2(0.5f * z.x, -0.5f * z.y);          // conj(Z)
+}
+
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
                                                       Pass p, Tables T, int batch, long long C) {
@@ -207,24 +221,28 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
-    const int nbm = (1 << p.lgnb) - 1, S = seq_stride(p.lgnb);
-    const int n2a = tile << p.lgnb;
-    const int cols = min(nbm + 1, p.L2 - n2a);
-    const int tot = p.L1 << p.lgnb;
+    const int nb = 1 << p.lgnb, S = seq_stride(p.lgnb);
+    const bool pair = nb >= 2;
+    const int lgH = pair ? p.lgnb - 1 : 0, H = 1 << lgH;
+    const int c0 = tile << lgH;                                      // first primary column
+    const int ncols = min(H, (pair ? (p.L2 >> 1) + 1 : p.L2) - c0);  // primary columns here
+    const int tot = p.L1 << lgH;
     const float2* Ws = W + (long long)sig * C;
-    // U elements at a time: the bin records of q and L - q, then the W values
-    // they name, then the retangle; indices are clamped into the tile
+    // U elements at a time: the bin records of q and L - q and both twiddles,
+    // then the W values they name, then the retangles; indices are clamped
+    // into the tile
     constexpr int U = 4;
     for (int base = threadIdx.x; base < tot; base += U * NT) {
         int4 gq[U], gm[U];
-        float2 om[U];
+        float2 oq[U], om[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int e = min(base + u * NT, tot - 1);
-            const int q = __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1);
+            const int q = __mul24(e >> lgH, p.L2) + c0 + min(e & (H - 1), ncols - 1);
             gq[u] = T.gather[q];
             gm[u] = T.gather[p.L - q];
-            om[u] = T.omega[q];                                   // (cos, -sin)
+            oq[u] = T.omega[q];
+            om[u] = T.omega[p.L - q];
         }
         float2 xq[U], xm[U];
 #pragma unroll
@@ -235,17 +253,13 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int e = base + u * NT;
-            if (e < tot) {
-                const int c = e & nbm, n1 = e >> p.lgnb;
-                float2 v = make_float2(0.f, 0.f);
-                if (c < cols) {
-                    if (n1 == 0 && n2a + c == 0) { xq[u].y = 0.f; xm[u].y = 0.f; }
-                    const float2 pa = make_float2(1.f + om[u].y, om[u].x);    // 1 + i conj(w)
-                    const float2 pb = make_float2(1.f - om[u].y, -om[u].x);   // 1 - i conj(w)
-                    const float2 zq = cadd(cmul(pa, xq[u]), cmul(pb, conjf2(xm[u])));
-                    v = make_float2(0.5f * zq.x, -0.5f * zq.y);               // conj(Z_q)
-                }
-                buf[__mul24(n1, S) + c] = v;
+            const int c = e & (H - 1), n1 = e >> lgH;
+            if (e < tot && c < ncols) {
+                const int n2 = c0 + c;
+                if (n1 == 0 && n2 == 0) { xq[u].y = 0.f; xm[u].y = 0.f; }    // DC and Nyquist
+                buf[__mul24(n1, S) + c] = retangle_conj(oq[u], xq[u], xm[u]);
+                if (pair && n2 != 0 && 2 * n2 != p.L2)
+                    buf[__mul24(p.L1 - 1 - n1, S) + H + c] = retangle_conj(om[u], xm[u], xq[u]);
             }
         }
     }
@@ -253,11 +267,13 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
-    for (int e = threadIdx.x; e < tot; e += NT) {
-        const int c = e & nbm, k1 = e >> p.lgnb;
-        if (c < cols) {
-            const int n2 = n2a + c;
-            Ys[__mul24(k1, p.L2) + n2] = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
+    for (int e = threadIdx.x; e < (p.L1 << p.lgnb); e += NT) {
+        const int slot = e & (nb - 1), k1 = e >> p.lgnb;
+        const int c = slot & (H - 1), n2 = c0 + c;
+        const bool mirror = pair && slot >= H;
+        if (c < ncols && !(mirror && (n2 == 0 || 2 * n2 == p.L2))) {
+            const int col = mirror ? p.L2 - n2 : n2;
+            Ys[__mul24(k1, p.L2) + col] = cmul(buf[__mul24(k1, S) + slot], tw4(t4, p, __mul24(col, k1)));
         }
     }
 }

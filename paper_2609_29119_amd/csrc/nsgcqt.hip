@@ -199,7 +199,14 @@ int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl
 }
 
 int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream_t s) {
-    const Pass q = pass_a(p->h);
+    Pass q = pass_a(p->h);
+    // tiles of 2^(lgnb-1) primary columns in [0, L2/2] and their mirrors
+    if (q.lgnb >= 1) {
+        const int H = 1 << (q.lgnb - 1);
+        q.ntile = (q.L2 / 2 + 1 + H - 1) / H;
+    } else {
+        q.ntile = q.L2;
+    }
     const int lds = lds_pass_a(q);
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
