@@ -73,6 +73,19 @@ __device__ __forceinline__ float2 tw_at(const TwL& w, int t) {
     return cmul(w.t[t >> w.lg], w.t[w.nhi + (t & ((1 << w.lg) - 1))]);
 }
 
+// Element idx of base through a 32-bit byte offset. With base uniform across
+// the wave this is the scalar-base + vector-offset address form, which saves
+// the 64-bit address arithmetic per access. The plan keeps every offset used
+// this way below 2^32 bytes.
+template <class T>
+__device__ __forceinline__ const T& at32(const T* base, uint32_t idx) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + idx * static_cast<uint32_t>(sizeof(T)));
+}
+template <class T>
+__device__ __forceinline__ T& at32(T* base, uint32_t idx) {
+    return *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + idx * static_cast<uint32_t>(sizeof(T)));
+}
+
 // ---------------------------------------------------------------- butterflies
 // Forward DFTs of length R on v[0..R-1], in registers.
 
@@ -283,9 +296,9 @@ __device__ __forceinline__ void prime_fold(float2* buf, int n, int S, int lgnb, 
             if (Ns > 1) {
                 int k;
                 qdiv(jj, dns, k);
-                const float2* w = tws + __mul24(k, R - 1);
-                wa[u] = w[r - 1];
-                wc[u] = w[R - r - 1];
+                const int w0 = __mul24(k, R - 1) - 1;
+                wa[u] = at32(tws, w0 + r);
+                wc[u] = at32(tws, w0 + R - r);
             }
         }
 #pragma unroll

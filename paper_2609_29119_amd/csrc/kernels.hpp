@@ -135,7 +135,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
         const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
         load_phase<NT, 4>(
             tot,
-            [&](int e) { return z[__mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1)]; },
+            [&](int e) { return at32(z, __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1)); },
             [&](int e, float2 v) {
                 const int c = e & nbm;
                 buf[__mul24(e >> p.lgnb, S) + c] = c < cols ? v : make_float2(0.f, 0.f);
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
         const int c = e & nbm, k1 = e >> p.lgnb;
         if (c < cols) {
             const int n2 = n2a + c;
-            Ys[__mul24(k1, p.L2) + n2] = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
+            at32(Ys, __mul24(k1, p.L2) + n2) = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
         }
     }
 }
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
 __device__ __forceinline__ float4 make_float4_2(float2 a, float2 b) { return make_float4(a.x, a.y, b.x, b.y); }
 
 __device__ __forceinline__ float2 gather_bin(const float2* __restrict__ Ws, int4 g) {
-    const float2 a = Ws[g.x], b = Ws[g.y], c = Ws[g.z];
+    const float2 a = at32(Ws, g.x), b = at32(Ws, g.y), c = at32(Ws, g.z);
     // masks instead of branches, so the compiler cannot sink the reads
     const float mb = g.w > 1 ? 1.f : 0.f, mc = g.w > 2 ? 1.f : 0.f;
     return make_float2(a.x + mb * b.x + mc * c.x, a.y + mb * b.y + mc * c.y);
@@ -239,10 +239,10 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
         for (int u = 0; u < U; ++u) {
             const int e = min(base + u * NT, tot - 1);
             const int q = __mul24(e >> lgH, p.L2) + c0 + min(e & (H - 1), ncols - 1);
-            gq[u] = T.gather[q];
-            gm[u] = T.gather[p.L - q];
-            oq[u] = T.omega[q];
-            om[u] = T.omega[p.L - q];
+            gq[u] = at32(T.gather, q);
+            gm[u] = at32(T.gather, p.L - q);
+            oq[u] = at32(T.omega, q);
+            om[u] = at32(T.omega, p.L - q);
         }
         float2 xq[U], xm[U];
 #pragma unroll
@@ -267,14 +267,17 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
     __syncthreads();
     float2* Ys = Y + (long long)sig * p.L;
-    for (int e = threadIdx.x; e < (p.L1 << p.lgnb); e += NT) {
-        const int slot = e & (nb - 1), k1 = e >> p.lgnb;
+    // output column of a slot (primary or mirror), -1 for an unused slot
+    auto column = [&](int slot) {
         const int c = slot & (H - 1), n2 = c0 + c;
         const bool mirror = pair && slot >= H;
-        if (c < ncols && !(mirror && (n2 == 0 || 2 * n2 == p.L2))) {
-            const int col = mirror ? p.L2 - n2 : n2;
-            Ys[__mul24(k1, p.L2) + col] = cmul(buf[__mul24(k1, S) + slot], tw4(t4, p, __mul24(col, k1)));
-        }
+        if (c >= ncols || (mirror && (n2 == 0 || 2 * n2 == p.L2))) return -1;
+        return mirror ? p.L2 - n2 : n2;
+    };
+    for (int e = threadIdx.x; e < (p.L1 << p.lgnb); e += NT) {
+        const int slot = e & (nb - 1), k1 = e >> p.lgnb;
+        const int col = column(slot);
+        if (col >= 0) at32(Ys, __mul24(k1, p.L2) + col) = cmul(buf[__mul24(k1, S) + slot], tw4(t4, p, __mul24(col, k1)));
     }
 }
 
@@ -301,7 +304,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
     // rows past the last one are read clamped and stored as zeros
     const int last = __mul24(rows, p.L2) - 1;
     load_phase<NT, 4>(
-        tot, [&](int e) { return Ys[min(e, last)]; },
+        tot, [&](int e) { return at32(Ys, min(e, last)); },
         [&](int e, float2 v) {
             int n2;
             const int r = qdiv(e, dl2, n2);
@@ -314,25 +317,12 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict_
         const int r = e & nbm, k2 = e >> p.lgnb;
         if (r < rows) {
             const float2 v = buf[__mul24(k2, S) + r];
-            os[k1a + r + __mul24(p.L1, k2)] = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
+            at32(os, k1a + r + __mul24(p.L1, k2)) = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
         }
     }
 }
 
 // ------------------------------------------------------------ band analysis
-// Element idx of base through a 32-bit byte offset. With base uniform across
-// the wave this is the scalar-base + vector-offset address form, which saves
-// the 64-bit address arithmetic per access. The plan keeps every offset used
-// this way below 2^32 bytes.
-template <class T>
-__device__ __forceinline__ const T& at32(const T* base, uint32_t idx) {
-    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + idx * static_cast<uint32_t>(sizeof(T)));
-}
-template <class T>
-__device__ __forceinline__ T& at32(T* base, uint32_t idx) {
-    return *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + idx * static_cast<uint32_t>(sizeof(T)));
-}
-
 // Entries of nb = 2^lg interleaved sequences of length n: thread tid owns
 // sequence tid & (nb - 1) and its entries i = (tid >> lg) + j (NT >> lg) < n,
 // U at a time; as in load_phase, all U gets are issued before the first put,

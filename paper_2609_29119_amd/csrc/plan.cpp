@@ -35,7 +35,7 @@ int smallest_prime_factor(int64_t n) {
     return static_cast<int>(n);
 }
 
-// Forward DFT (eq. 1) of a 7-smooth length in fp64, recursive decimation in
+// Forward DFT (eq. 1) of a smooth length in fp64, recursive decimation in
 // time. Used only at plan time for the Bluestein kernels.
 void host_dft(std::vector<cd>& x) {
     const int64_t n = static_cast<int64_t>(x.size());
@@ -51,16 +51,6 @@ void host_dft(std::vector<cd>& x) {
         for (int r = 0; r < p; ++r) acc += sub[r][k % m] * root(static_cast<int64_t>(r) * k, n);
         x[k] = acc;
     }
-}
-
-int64_t smooth7_at_least(int64_t target) {
-    int64_t best = INT64_MAX;
-    for (int64_t a = 1; a < 4 * target; a *= 2)
-        for (int64_t b = a; b < 4 * target; b *= 3)
-            for (int64_t c = b; c < 4 * target; c *= 5)
-                for (int64_t d = c; d < 4 * target; d *= 7)
-                    if (d >= target && d < best) best = d;
-    return best;
 }
 
 void push_c(std::vector<float>& v, cd z) {
@@ -264,6 +254,29 @@ double band_fft_cost(int64_t n, int64_t row_bytes) {
     const int lg = seq_lg(n, t.nt * t.ept, 1 << 30, row_bytes);
     if (!mfma_fits(rad, n, lg, t.nt)) return std::numeric_limits<double>::infinity();
     return stage_cost(rad, n, lg);
+}
+
+// Bluestein length for a band of length M: among the P >= 2M - 1 (up to a
+// quarter longer) whose prime factors are all compile-time radices (2..13),
+// the one with the lowest estimated cost of two length-P transforms and the
+// three pointwise products; *cost receives that cost.
+int64_t bluestein_length(int64_t M, int64_t row_bytes, double* cost) {
+    const int64_t lo = 2 * M - 1, hi = lo + lo / 4 + 16;
+    int64_t best = -1;
+    double best_c = std::numeric_limits<double>::infinity();
+    for (int64_t P = lo; P <= hi; ++P) {
+        int64_t m = P;
+        for (int q : {2, 3, 5, 7, 11, 13})
+            while (m % q == 0) m /= q;
+        if (m != 1) continue;
+        const double c = 2.0 * band_fft_cost(P, row_bytes) + 0.6 * static_cast<double>(P);
+        if (c < best_c) {
+            best_c = c;
+            best = P;
+        }
+    }
+    *cost = best_c;
+    return best;
 }
 
 }  // namespace
@@ -480,7 +493,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         for (int64_t j = 0; j < s; ++j) push_c(p.tw4_lo, root(j, L));
     }
 
-    // ---- band transforms: mixed radix, or Bluestein over a 7-smooth length
+    // ---- band transforms: mixed radix, or Bluestein over a smooth length
     p.banddev.clear(); p.chirp.clear(); p.kern.clear();
     const int64_t row_bytes = std::max<int64_t>(p.L + 1, p.C) * 8;
     std::vector<int> work(p.bands.size());
@@ -496,10 +509,10 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         // direct transform of length M, or Bluestein over P, whichever the
         // cost model prefers
         const int64_t M = b.M;
-        const int64_t P = smooth7_at_least(2 * M - 1);
+        double c_blu = 0.0;
+        const int64_t P = bluestein_length(M, row_bytes, &c_blu);
         const double c_direct = band_fft_cost(M, row_bytes);
-        const double c_blu = 2.0 * band_fft_cost(P, row_bytes) + 0.6 * static_cast<double>(P);
-        if (c_direct <= c_blu) {
+        if (c_direct <= c_blu || P < 0) {
             d.fft = reg.get(M);
             if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no radix plan for a band");
             work[l] = static_cast<int>(M);

@@ -10,8 +10,8 @@ namespace nsg {
 // cores, which form the stage's outputs as products with the cosine and sine
 // matrices of the prime. Band lengths with a larger prime factor, or whose
 // stage does not fit a workgroup's matrix tiles, are transformed with
-// Bluestein's chirp-z algorithm over a 7-smooth length P >= 2M - 1, which is
-// also used where the cost model finds it cheaper.
+// Bluestein's chirp-z algorithm over a length P >= 2M - 1 with prime factors
+// up to 13, which is also used where the cost model finds it cheaper.
 constexpr int kMfmaMaxRadix = 257;
 constexpr int kMaxStages = 24;
 // 16 x 16 result tiles one wave keeps in registers across the barrier of a
