@@ -433,15 +433,17 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
 // by every workgroup of the same length, so they stay in the caches). The
 // plan guarantees that every prime-radix stage's result tiles fit the
 // workgroup. Ends with a barrier when there is a stage.
+// `stw` points at this length's stage twiddles: pool + d->stw, or a copy
+// of them (d->ntw values) in LDS.
 template <int NT, int EPT>
 __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftDesc* __restrict__ d,
-                                        const float2* __restrict__ pool) {
+                                        const float2* __restrict__ pool, const float2* __restrict__ stw) {
     const int n = d->n;
     const int ns = d->nstages;
     int Ns = 1;
     for (int s = 0; s < ns; ++s) {
         const int R = d->radix[s];
-        const float2* tw = pool + d->stw + d->stoff[s];
+        const float2* tw = stw + d->stoff[s];
         switch (R) {
             case 2: stage_fixed<2, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
             case 3: stage_fixed<3, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
@@ -464,6 +466,12 @@ __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftD
         }
         Ns *= R;
     }
+}
+
+template <int NT, int EPT>
+__device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftDesc* __restrict__ d,
+                                        const float2* __restrict__ pool) {
+    lds_fft<NT, EPT>(buf, S, lgnb, d, pool, pool + d->stw);
 }
 
 // Interleave stride of nb = 2^lgnb sequences.

@@ -13,6 +13,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "fft_lds.hpp"
 
 namespace nsg {
@@ -116,66 +118,90 @@ __device__ __forceinline__ float2 tw4(const float2* t4, const Pass& p, int t) {
 // -------------------------------------------------- packed FFT, pass A (columns)
 // Loads z_j = x_{2j} + i x_{2j+1} (eq. 5) for j = n1 L2 + n2 over a tile of
 // columns n2, runs the length-L1 column DFTs, multiplies by omega_L^{n2 k1} and
-// writes Y[k1 L2 + n2].
-template <int NT, int EPT>
+// writes Y[k1 L2 + n2]. SLICED: z_j comes from slice s0 + sig of a long
+// signal, windowed (Sec. 4). Persistent like pass B: the descriptor, stage
+// twiddles and four-step twiddles sit in LDS, and the next tile's inputs are
+// read into registers while the current tile is transformed.
+template <int NT, int EPT, bool SLICED>
 __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ x, float2* __restrict__ Y,
                                                       Pass p, Tables T, SliceIn sl, int batch, long long sig_stride) {
     extern __shared__ float2 lds[];
+    __shared__ FftDesc fdl;
+    const FftDesc* fd = T.ffts + p.fft;
     float2 *t4, *buf;
     pass_lds(lds, p, true, t4, buf);
+    float2* twl = buf;
+    buf += p.ntw;
+    for (int i = threadIdx.x; i < static_cast<int>(sizeof(FftDesc) / 4); i += NT)
+        reinterpret_cast<int*>(&fdl)[i] = reinterpret_cast<const int*>(fd)[i];
+    for (int i = threadIdx.x; i < p.ntw; i += NT) twl[i] = T.tw[fd->stw + i];
     load_tw4<NT>(t4, p, T);
     const int G = p.ntile * batch;
-    const int lid = xcd_remap(blockIdx.x, G);
-    const int tile = lid % p.ntile, sig = lid / p.ntile;
     const int nbm = (1 << p.lgnb) - 1, S = seq_stride(p.lgnb);
-    const int n2a = tile << p.lgnb;
-    const int cols = min(nbm + 1, p.L2 - n2a);
     const int tot = p.L1 << p.lgnb;
-    if (!sl.enabled) {
-        const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
-        load_phase<NT, 4>(
-            tot,
-            [&](int e) { return at32(z, __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1)); },
-            [&](int e, float2 v) {
-                const int c = e & nbm;
-                buf[__mul24(e >> p.lgnb, S) + c] = c < cols ? v : make_float2(0.f, 0.f);
-            });
-    } else {
-        // padded coordinate of sample 2j of slice s is s H + 2j; the signal
-        // starts at padded H. Reads are clamped into the signal and masked.
-        const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
-        const long long last = sl.n - 1;
-        load_phase<NT, 4>(
-            tot,
-            [&](int e) {
-                const int j = __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cols - 1);
-                const long long t = base + 2 * (long long)j;
-                const long long t0 = t < 0 ? 0 : (t > last ? last : t);
-                const long long t1 = t + 1 < 0 ? 0 : (t + 1 > last ? last : t + 1);
-                return make_float4(x[t0], x[t1], T.slicewin[2 * j], T.slicewin[2 * j + 1]);
-            },
-            [&](int e, float4 r) {
+    // per element: (x_2j, x_2j+1) or, sliced, the two samples and their window
+    using Pre = typename std::conditional<SLICED, float4, float2>::type;
+    Pre pre[EPT];
+    // padded coordinate of sample 2j of slice s is s H + 2j; the signal
+    // starts at padded H. Reads are clamped into the tile and the signal.
+    auto fetch = [&](int t) {
+        const int tile = t % p.ntile, sig = t / p.ntile;
+        const int n2a = tile << p.lgnb;
+        const int cmax = min(nbm + 1, p.L2 - n2a) - 1;
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int e = min(static_cast<int>(threadIdx.x) + u * NT, tot - 1);
+            const int j = __mul24(e >> p.lgnb, p.L2) + n2a + min(e & nbm, cmax);
+            if constexpr (SLICED) {
+                const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
+                const long long tt = base + 2 * (long long)j;
+                const long long last = sl.n - 1;
+                const long long t0 = tt < 0 ? 0 : (tt > last ? last : tt);
+                const long long t1 = tt + 1 < 0 ? 0 : (tt + 1 > last ? last : tt + 1);
+                pre[u] = make_float4(x[t0], x[t1], T.slicewin[2 * j], T.slicewin[2 * j + 1]);
+            } else {
+                const float2* z = reinterpret_cast<const float2*>(x + (long long)sig * sig_stride);
+                pre[u] = at32(z, j);
+            }
+        }
+    };
+    int t = blockIdx.x;
+    if (t < G) fetch(t);
+    for (; t < G; t += gridDim.x) {
+        const int tile = t % p.ntile, sig = t / p.ntile;
+        const int n2a = tile << p.lgnb;
+        const int cols = min(nbm + 1, p.L2 - n2a);
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int e = threadIdx.x + u * NT;
+            if (e < tot) {
                 const int c = e & nbm, n1 = e >> p.lgnb;
-                const int j = __mul24(n1, p.L2) + n2a + c;
-                const long long t = base + 2 * (long long)j;
                 float2 v = make_float2(0.f, 0.f);
                 if (c < cols) {
-                    if (t >= 0 && t < sl.n) v.x = r.x * r.z;
-                    if (t + 1 >= 0 && t + 1 < sl.n) v.y = r.y * r.w;
+                    if constexpr (SLICED) {
+                        const long long base = (long long)(sl.s0 + sig) * sl.H - sl.H;
+                        const long long tt = base + 2 * (long long)(__mul24(n1, p.L2) + n2a + c);
+                        if (tt >= 0 && tt < sl.n) v.x = pre[u].x * pre[u].z;
+                        if (tt + 1 >= 0 && tt + 1 < sl.n) v.y = pre[u].y * pre[u].w;
+                    } else {
+                        v = pre[u];
+                    }
                 }
                 buf[__mul24(n1, S) + c] = v;
-            });
-    }
-    __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
-    __syncthreads();
-    float2* Ys = Y + (long long)sig * p.L;
-    for (int e = threadIdx.x; e < tot; e += NT) {
-        const int c = e & nbm, k1 = e >> p.lgnb;
-        if (c < cols) {
-            const int n2 = n2a + c;
-            at32(Ys, __mul24(k1, p.L2) + n2) = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
+            }
         }
+        __syncthreads();
+        if (t + static_cast<int>(gridDim.x) < G) fetch(t + gridDim.x);
+        lds_fft<NT, EPT>(buf, S, p.lgnb, &fdl, T.tw, twl);
+        float2* Ys = Y + (long long)sig * p.L;
+        for (int e = threadIdx.x; e < tot; e += NT) {
+            const int c = e & nbm, k1 = e >> p.lgnb;
+            if (c < cols) {
+                const int n2 = n2a + c;
+                at32(Ys, __mul24(k1, p.L2) + n2) = cmul(buf[__mul24(k1, S) + c], tw4(t4, p, __mul24(n2, k1)));
+            }
+        }
+        __syncthreads();
     }
 }
 
@@ -285,40 +311,65 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
 // Row k1 of Y (length L2) is transformed; output k = k1 + L1 k2.
 // INVERSE = false: Z[k] = result (natural order).
 // INVERSE = true : z_k = conj(result) / L, unpacked to x_{2k}, x_{2k+1} (P^{-1}).
+// Persistent: workgroup w takes tiles w, w + gridDim.x, ... (tile = 2^lgnb
+// rows of one signal). The stage twiddles of length L2 sit in LDS, so the
+// only global reads are the tiles': the next tile's rows are read into
+// registers while the current tile is transformed.
 template <int NT, int EPT, bool INVERSE>
 __global__ __launch_bounds__(NT) NSG_OCC void k_pass_b(const float2* __restrict__ Y, float2* __restrict__ out,
                                                        Pass p, Tables T, int batch, long long out_stride,
                                                        float inv_L) {
     extern __shared__ float2 lds[];
-    float2 *t4, *buf;
-    pass_lds(lds, p, false, t4, buf);
+    // the descriptor and stage twiddles are read from LDS inside the loop:
+    // any global read there would have to wait for the prefetched rows first
+    __shared__ FftDesc fdl;
+    const FftDesc* fd = T.ffts + p.fft;
+    float2* twl = lds;
+    float2* buf = lds + p.ntw;
+    for (int i = threadIdx.x; i < static_cast<int>(sizeof(FftDesc) / 4); i += NT)
+        reinterpret_cast<int*>(&fdl)[i] = reinterpret_cast<const int*>(fd)[i];
+    for (int i = threadIdx.x; i < p.ntw; i += NT) twl[i] = T.tw[fd->stw + i];
     const int G = p.ntile * batch;
-    const int lid = xcd_remap(blockIdx.x, G);
-    const int tile = lid % p.ntile, sig = lid / p.ntile;
     const int nbm = (1 << p.lgnb) - 1, S = seq_stride(p.lgnb);
-    const int k1a = tile << p.lgnb;
-    const int rows = min(nbm + 1, p.L1 - k1a);
     const int tot = p.L2 << p.lgnb;
     const Div dl2 = mkdiv(p.L2);
-    const float2* Ys = Y + (long long)sig * p.L + (long long)k1a * p.L2;
-    // rows past the last one are read clamped and stored as zeros
-    const int last = __mul24(rows, p.L2) - 1;
-    load_phase<NT, 4>(
-        tot, [&](int e) { return at32(Ys, min(e, last)); },
-        [&](int e, float2 v) {
-            int n2;
-            const int r = qdiv(e, dl2, n2);
-            buf[__mul24(n2, S) + r] = r < rows ? v : make_float2(0.f, 0.f);
-        });
-    __syncthreads();
-    lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
-    float2* os = out + (long long)sig * out_stride;
-    for (int e = threadIdx.x; e < tot; e += NT) {
-        const int r = e & nbm, k2 = e >> p.lgnb;
-        if (r < rows) {
-            const float2 v = buf[__mul24(k2, S) + r];
-            at32(os, k1a + r + __mul24(p.L1, k2)) = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
+    float2 pre[EPT];
+    // rows past the tile's last one are read clamped and stored as zeros
+    auto fetch = [&](int t) {
+        const int tile = t % p.ntile, sig = t / p.ntile;
+        const int k1a = tile << p.lgnb;
+        const int last = __mul24(min(nbm + 1, p.L1 - k1a), p.L2) - 1;
+        const float2* Ys = Y + (long long)sig * p.L + (long long)k1a * p.L2;
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) pre[u] = at32(Ys, min(static_cast<int>(threadIdx.x) + u * NT, last));
+    };
+    int t = blockIdx.x;
+    if (t < G) fetch(t);
+    for (; t < G; t += gridDim.x) {
+        const int tile = t % p.ntile, sig = t / p.ntile;
+        const int k1a = tile << p.lgnb;
+        const int rows = min(nbm + 1, p.L1 - k1a);
+#pragma unroll
+        for (int u = 0; u < EPT; ++u) {
+            const int e = threadIdx.x + u * NT;
+            if (e < tot) {
+                int n2;
+                const int r = qdiv(e, dl2, n2);
+                buf[__mul24(n2, S) + r] = r < rows ? pre[u] : make_float2(0.f, 0.f);
+            }
         }
+        __syncthreads();
+        if (t + static_cast<int>(gridDim.x) < G) fetch(t + gridDim.x);
+        lds_fft<NT, EPT>(buf, S, p.lgnb, &fdl, T.tw, twl);
+        float2* os = out + (long long)sig * out_stride;
+        for (int e = threadIdx.x; e < tot; e += NT) {
+            const int r = e & nbm, k2 = e >> p.lgnb;
+            if (r < rows) {
+                const float2 v = buf[__mul24(k2, S) + r];
+                at32(os, k1a + r + __mul24(p.L1, k2)) = INVERSE ? make_float2(v.x * inv_L, -v.y * inv_L) : v;
+            }
+        }
+        __syncthreads();
     }
 }
 

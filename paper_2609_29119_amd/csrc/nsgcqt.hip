@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -47,6 +48,7 @@ struct nsgcqt_plan_s {
     const float* wSa = nullptr;
     std::vector<hipEvent_t> events;
     int ev_next = 0;
+    std::map<const void*, int> resident;   // persistent kernels: workgroups resident at once
 };
 
 namespace {
@@ -171,7 +173,23 @@ int lds_pass_a(const Pass& q) {
     return (q.nhi4 + (1 << q.split) + lds_slots(q.L1, q.lgnb)) * static_cast<int>(sizeof(float2));
 }
 int lds_pass_b(const Pass& q) {
-    return lds_slots(q.L2, q.lgnb) * static_cast<int>(sizeof(float2));
+    return (q.ntw + lds_slots(q.L2, q.lgnb)) * static_cast<int>(sizeof(float2));
+}
+
+// Workgroups of a persistent kernel that are resident on the device at once
+// (cached per plan and kernel); 0 if the runtime cannot say.
+template <typename K>
+int resident_blocks(nsgcqt_plan_s* p, K kernel, int nt, int lds) {
+    const void* key = reinterpret_cast<const void*>(kernel);
+    auto it = p->resident.find(key);
+    if (it != p->resident.end()) return it->second;
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, key, nt, lds) != hipSuccess)
+        return 0;
+    p->resident[key] = cus * per;
+    return cus * per;
 }
 
 #define DISPATCH_NT(nt, KERNEL, ...)                                                         \
@@ -184,17 +202,23 @@ int lds_pass_b(const Pass& q) {
 int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl, long long sig_stride,
               hipStream_t s) {
     const Pass q = pass_a(p->h);
-    const int lds = lds_pass_a(q);
+    const int lds = lds_pass_a(q) + q.ntw * static_cast<int>(sizeof(float2));   // + stage twiddles
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
+        const int tiles = q.ntile * batch;
+        const int res = resident_blocks(p, k, p->h.fs4.nt_a, lds);
+        const int grid = res > 0 ? std::min(tiles, res) : tiles;
         ev_start(p, s);
-        hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch,
-                           sig_stride);
+        hipLaunchKernelGGL(k, dim3(grid), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch, sig_stride);
         HIP_TRY(hipGetLastError());
         ev_end(p, s);
         return NSGCQT_OK;
     };
-    DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a)
+    if (sl.enabled) {
+        DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a, , true)
+    } else {
+        DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a, , false)
+    }
     return NSGCQT_OK;
 }
 
@@ -228,8 +252,11 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
     const float inv_L = static_cast<float>(1.0 / static_cast<double>(p->h.L));
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
+        const int tiles = q.ntile * batch;
+        const int res = resident_blocks(p, k, p->h.fs4.nt_b, lds);
+        const int grid = res > 0 ? std::min(tiles, res) : tiles;
         ev_start(p, s);
-        hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_b), lds, s, Y, out, q, p->T, batch,
+        hipLaunchKernelGGL(k, dim3(grid), dim3(p->h.fs4.nt_b), lds, s, Y, out, q, p->T, batch,
                            out_stride, inv_L);
         HIP_TRY(hipGetLastError());
         ev_end(p, s);

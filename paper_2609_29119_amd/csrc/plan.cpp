@@ -479,8 +479,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             int lg4 = 0;
             while ((int64_t(1) << (2 * lg4)) < L) ++lg4;
             const int64_t t4 = ((L + (int64_t(1) << lg4) - 1) >> lg4) + (int64_t(1) << lg4);
-            const int64_t a_slots = t4 + lds_slots(static_cast<int>(f.L1), f.tile_a);
-            const int64_t b_slots = lds_slots(static_cast<int>(f.L2), f.tile_b);
+            const int64_t a_slots = t4 + p.ffts[f.fft1].ntw + lds_slots(static_cast<int>(f.L1), f.tile_a);
+            const int64_t b_slots = p.ffts[f.fft2].ntw + lds_slots(static_cast<int>(f.L2), f.tile_b);
             if (a_slots * 8 > 160 * 1024 || b_slots * 8 > 160 * 1024)
                 return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds LDS");
         }
