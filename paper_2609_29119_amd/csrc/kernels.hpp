@@ -22,6 +22,9 @@ namespace nsg {
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
 // caps each kernel at 256 VGPRs per lane.
 #define NSG_OCC __attribute__((amdgpu_waves_per_eu(2)))
+// The 256 x 8 band kernels carry most of the band work and gain from six
+// waves per SIMD (at most 80 VGPRs, no spills); the others do not.
+#define NSG_OCC_BAND __attribute__((amdgpu_waves_per_eu((NT == 256 && EPT == 8) ? 6 : 2)))
 
 struct Tables {
     const BandDev* bands;
@@ -417,7 +420,7 @@ __device__ __forceinline__ void blu_middle(float2* buf, int n, int lg, int S, in
 // F_M v = ch * conj(F_P conj(F_P(ch v) * K)) where K = F_P(b)/P and b the
 // cyclic chirp exp(+i pi t^2/M), |t| < M.
 template <int NT, int EPT>
-__global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __restrict__ Z, float2* __restrict__ coef,
+__global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2* __restrict__ Z, float2* __restrict__ coef,
                                                               const float* __restrict__ wt, Tables T, int item0,
                                                               int nitems, int batch, int L, long long C) {
     extern __shared__ float2 lds[];
@@ -493,7 +496,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_band_analysis(const float2* __re
 // T^dagger weight for T^dagger). Overlapping bands are summed later by the
 // owner of each bin.
 template <int NT, int EPT>
-__global__ __launch_bounds__(NT) NSG_OCC void k_band_synthesis(const float2* __restrict__ coef, float2* __restrict__ W,
+__global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2* __restrict__ coef, float2* __restrict__ W,
                                                                const float* __restrict__ wt, Tables T, int item0,
                                                                int nitems, int batch, long long C) {
     extern __shared__ float2 lds[];
