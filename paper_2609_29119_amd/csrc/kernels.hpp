@@ -424,7 +424,7 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                                                               const float* __restrict__ wt, Tables T, int item0,
                                                               int nitems, int batch, int L, long long C) {
     extern __shared__ float2 lds[];
-    const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
+    const WorkItem it = T.items[item0 + blockIdx.x];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
@@ -500,7 +500,7 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
                                                                const float* __restrict__ wt, Tables T, int item0,
                                                                int nitems, int batch, long long C) {
     extern __shared__ float2 lds[];
-    const WorkItem it = T.items[item0 + xcd_remap(blockIdx.x, nitems)];
+    const WorkItem it = T.items[item0 + blockIdx.x];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
