@@ -27,17 +27,24 @@ HBM_PEAK = 8.0e12          # MI355X HBM3E, bytes/s
 METRIC = "CQT analysis+synthesis round-trip audio samples/s and % HBM peak; round-trip SNR dB"
 
 
+# hipEventDisableSystemFence: timing-only events skip the system-scope cache
+# writeback and invalidation at record, which would otherwise add to (and
+# perturb) the bracketed kernel's measured time
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
 class HipEvents:
     """A few HIP events through the runtime's C API (timing only)."""
 
     def __init__(self, n):
         self.rt = ctypes.CDLL("libamdhip64.so")
         self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         self.ev = []
         for _ in range(n):
             e = ctypes.c_void_p()
-            if self.rt.hipEventCreate(ctypes.byref(e)) != 0:
-                raise RuntimeError("hipEventCreate failed")
+            if self.rt.hipEventCreateWithFlags(ctypes.byref(e), HIP_EVENT_DISABLE_SYSTEM_FENCE) != 0:
+                raise RuntimeError("hipEventCreateWithFlags failed")
             self.ev.append(e.value)
 
     def elapsed_ms(self, a, b):
