@@ -89,6 +89,10 @@ typedef struct {
     double centre_hz;   /* 0 for DC, fs/2 for Nyquist */
     double xi;          /* centre in bins (unrounded) of the governing Hann window */
     double beta;        /* its half-amplitude width in bins */
+    int64_t fft_len;    /* length of the band's DFT as evaluated: M for a direct
+                           mixed-radix transform, P >= 2M - 1 for Bluestein */
+    int64_t bluestein;  /* 1 if the band uses Bluestein's algorithm (two
+                           length-P transforms), 0 otherwise; independent of batch */
 } nsgcqt_band;
 
 typedef struct {
@@ -116,9 +120,12 @@ typedef struct {
  * EINVAL: out NULL, N odd or < 4, fs <= 0, fmin <= 0, fmin >= fs/2,
  *         fmax < fmin, bins_per_octave < 1, batch < 1, or a bin that no band
  *         covers (a_k = 0, Sec. 2).
- * EUNSUPPORTED: L = N/2 has a prime factor above the largest radix of the
- *         packed FFT, or a band needs a transform larger than one workgroup's
- *         LDS can hold. */
+ * EUNSUPPORTED: N >= 2^29 (rows are addressed with 32-bit byte offsets);
+ *         L = N/2 has a prime factor above 257, the largest Stockham radix;
+ *         or a band transform beyond one workgroup has no split n = n1 n2
+ *         with n1 <= n2 <= 4096 into such radices. Bands never need their
+ *         length's prime factors to be small: Bluestein's algorithm covers
+ *         any length. */
 int nsgcqt_plan_create(nsgcqt_plan* out, double fs, double fmin, double fmax,
                        int bins_per_octave, int64_t n_samples, int batch);
 

@@ -482,6 +482,9 @@ int nsgcqt_band_info(nsgcqt_plan p, int band, nsgcqt_band* o) {
     o->centre_hz = b.f;
     o->xi = b.xi;
     o->beta = b.beta;
+    const BandDev& d = p->h.banddev[band];
+    o->fft_len = p->h.ffts[d.fft].n;
+    o->bluestein = d.chirp >= 0 ? 1 : 0;
     return NSGCQT_OK;
 }
 

@@ -47,7 +47,8 @@ class Info(ctypes.Structure):
 class BandInfo(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int64), ("k_lo", ctypes.c_int64), ("k_hi", ctypes.c_int64),
                 ("k_centre", ctypes.c_int64), ("length", ctypes.c_int64), ("offset", ctypes.c_int64),
-                ("centre_hz", ctypes.c_double), ("xi", ctypes.c_double), ("beta", ctypes.c_double)]
+                ("centre_hz", ctypes.c_double), ("xi", ctypes.c_double), ("beta", ctypes.c_double),
+                ("fft_len", ctypes.c_int64), ("bluestein", ctypes.c_int64)]
 
 
 _lib = None

@@ -177,6 +177,45 @@ def test_empty_bands_dropped_identically(lib):
     assert np.all(lay.a > 0)
 
 
+def _prime_factors(n):
+    out, m, d = [], n, 2
+    while d * d <= m:
+        while m % d == 0:
+            out.append(d)
+            m //= d
+        d += 1
+    if m > 1:
+        out.append(m)
+    return out
+
+
+@pytest.mark.parametrize("name", ["stress", "train"])
+def test_band_transform_choice(name):
+    """Per band, a direct transform of length M (prime factors up to the
+    largest Stockham radix, 257) or Bluestein over P >= 2M - 1 with prime
+    factors up to 13; the choice does not depend on the batch size."""
+    w = workloads.WORKLOADS[name]
+    p1 = nb.Plan(*w.plan_args, batch=1, device=False)
+    pb = nb.Plan(*w.plan_args, batch=w.batch, device=False)
+    b1, bb = p1.bands(), pb.bands()
+    assert [(b.fft_len, b.bluestein) for b in b1] == [(b.fft_len, b.bluestein) for b in bb]
+    for b in bb:
+        if b.bluestein:
+            assert b.fft_len >= 2 * b.length - 1
+            assert max(_prime_factors(b.fft_len)) <= 13
+        else:
+            assert b.fft_len == b.length
+            assert max(_prime_factors(b.length) + [1]) <= 257
+    assert all(b.bluestein for b in bb if max(_prime_factors(b.length) + [1]) > 257)
+    assert any(b.bluestein for b in bb) and any(not b.bluestein for b in bb)
+
+
+def test_size_limit(lib):
+    # rows are addressed with 32-bit byte offsets: N below 2^29
+    st, _ = _status(lib.nsgcqt_plan_create_host, 44100.0, 30.0, 22050.0, 12, 1 << 29, 1)
+    assert st == nb.EUNSUPPORTED
+
+
 def test_unsupported_packed_length(lib):
     # L = 2 * 263 has a prime factor above the largest Stockham radix (257)
     st, _ = _status(lib.nsgcqt_plan_create_host, 1052.0, 4.0, 526.0, 4, 1052, 1)
