@@ -257,13 +257,13 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     const int ncols = min(H, (pair ? (p.L2 >> 1) + 1 : p.L2) - c0);  // primary columns here
     const int tot = p.L1 << lgH;
     const float2* Ws = W + (long long)sig * C;
-    // U elements at a time: the bin records of q and L - q and both twiddles,
-    // then the W values they name, then the retangles; indices are clamped
+    // U elements at a time: the bin records of q and L - q and the twiddle of
+    // q, then the W values they name, then the retangles; indices are clamped
     // into the tile
     constexpr int U = 4;
     for (int base = threadIdx.x; base < tot; base += U * NT) {
         int4 gq[U], gm[U];
-        float2 oq[U], om[U];
+        float2 oq[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int e = min(base + u * NT, tot - 1);
@@ -271,7 +271,6 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
             gq[u] = at32(T.gather, q);
             gm[u] = at32(T.gather, p.L - q);
             oq[u] = at32(T.omega, q);
-            om[u] = at32(T.omega, p.L - q);
         }
         float2 xq[U], xm[U];
 #pragma unroll
@@ -287,8 +286,10 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
                 const int n2 = c0 + c;
                 if (n1 == 0 && n2 == 0) { xq[u].y = 0.f; xm[u].y = 0.f; }    // DC and Nyquist
                 buf[__mul24(n1, S) + c] = retangle_conj(oq[u], xq[u], xm[u]);
+                // omega_N^{L-q} = -conj(omega_N^q), as omega_N^L = -1
                 if (pair && n2 != 0 && 2 * n2 != p.L2)
-                    buf[__mul24(p.L1 - 1 - n1, S) + H + c] = retangle_conj(om[u], xm[u], xq[u]);
+                    buf[__mul24(p.L1 - 1 - n1, S) + H + c] =
+                        retangle_conj(make_float2(-oq[u].x, oq[u].y), xm[u], xq[u]);
             }
         }
     }
