@@ -442,32 +442,39 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
     const uint32_t zrow = static_cast<uint32_t>(live ? sg : 0) * static_cast<uint32_t>(L);
     const float2* chb = T.chirp + (blu ? bd.chirp : 0);   // entry 0 is valid in every table
     const float* w = wt + bd.off;
+    // the chirp is read only by Bluestein bands (a uniform branch around
+    // two instances of each phase)
     struct RouteIn { float2 za, zb, om, ch; float w; };
-    seq_phase<NT, 4>(
-        M, lg,
-        [&](int i) {
-            int slot = i + bd.rot;
-            if (slot >= M) slot -= M;
-            const int k = bd.k_lo + i;
-            const int a = (k == L) ? 0 : k;
-            const int bm = (a == 0) ? 0 : L - a;
-            return RouteIn{at32(Zb, zrow + a), at32(Zb, zrow + bm), at32(T.omega, k), at32(chb, blu ? slot : 0),
-                           at32(w, i)};
-        },
-        [&](int i, const RouteIn& r) {
-            int slot = i + bd.rot;
-            if (slot >= M) slot -= M;
-            float2 v = make_float2(0.f, 0.f);
-            if (live) {
-                const float2 pa = make_float2(1.f + r.om.y, -r.om.x);    // 1 - i w_k
-                const float2 pb = make_float2(1.f - r.om.y, r.om.x);     // 1 + i w_k
-                const float2 u2 = cadd(cmul(pa, r.za), cmul(pb, conjf2(r.zb)));
-                const float hw = 0.5f * r.w;
-                v = make_float2(hw * u2.x, -hw * u2.y);                  // conj(u)
-                if (blu) v = cmul(v, r.ch);
-            }
-            buf[__mul24(slot, S) + sg] = v;
-        });
+    auto route = [&](auto blu_t) {
+        constexpr bool BLU = decltype(blu_t)::value;
+        seq_phase<NT, 4>(
+            M, lg,
+            [&](int i) {
+                int slot = i + bd.rot;
+                if (slot >= M) slot -= M;
+                const int k = bd.k_lo + i;
+                const int a = (k == L) ? 0 : k;
+                const int bm = (a == 0) ? 0 : L - a;
+                return RouteIn{at32(Zb, zrow + a), at32(Zb, zrow + bm), at32(T.omega, k),
+                               BLU ? at32(chb, slot) : make_float2(1.f, 0.f), at32(w, i)};
+            },
+            [&](int i, const RouteIn& r) {
+                int slot = i + bd.rot;
+                if (slot >= M) slot -= M;
+                float2 v = make_float2(0.f, 0.f);
+                if (live) {
+                    const float2 pa = make_float2(1.f + r.om.y, -r.om.x);    // 1 - i w_k
+                    const float2 pb = make_float2(1.f - r.om.y, r.om.x);     // 1 + i w_k
+                    const float2 u2 = cadd(cmul(pa, r.za), cmul(pb, conjf2(r.zb)));
+                    const float hw = 0.5f * r.w;
+                    v = make_float2(hw * u2.x, -hw * u2.y);                  // conj(u)
+                    if (BLU) v = cmul(v, r.ch);
+                }
+                buf[__mul24(slot, S) + sg] = v;
+            });
+    };
+    if (blu) route(std::true_type{});
+    else route(std::false_type{});
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
@@ -481,14 +488,19 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
     if (!live) return;
     float2* cb = coef + (long long)it.s0 * C + bd.off;
     const uint32_t crow = static_cast<uint32_t>(sg) * static_cast<uint32_t>(C);
-    seq_phase<NT, 4>(
-        M, lg, [&](int i) { return at32(chb, blu ? i : 0); },
-        [&](int i, float2 chi) {
+    // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
+    if (blu) {
+        seq_phase<NT, 4>(
+            M, lg, [&](int i) { return at32(chb, i); },
+            [&](int i, float2 chi) {
+                at32(cb, crow + i) = cscale(cmul(conjf2(chi), buf[__mul24(i, S) + sg]), bd.inv_M);
+            });
+    } else {
+        for (int i = threadIdx.x >> lg; i < M; i += NT >> lg) {
             const float2 v = buf[__mul24(i, S) + sg];
-            // mixed radix: c = conj(V) / M; Bluestein: c = conj(ch * conj(D)) / M = conj(ch) D / M
-            at32(cb, crow + i) =
-                blu ? cscale(cmul(conjf2(chi), v), bd.inv_M) : make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
-        });
+            at32(cb, crow + i) = make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+        }
+    }
 }
 
 // ----------------------------------------------------------- band synthesis
@@ -515,16 +527,18 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
     const float2* chb = T.chirp + (blu ? bd.chirp : 0);   // entry 0 is valid in every table
     const float2* cb = coef + (long long)it.s0 * C + bd.off;
     const uint32_t crow = static_cast<uint32_t>(live ? sg : 0) * static_cast<uint32_t>(C);
-    seq_phase<NT, 4>(
-        M, lg, [&](int i) { return make_float4_2(at32(cb, crow + i), at32(chb, blu ? i : 0)); },
-        [&](int i, float4 r) {
-            float2 v = make_float2(0.f, 0.f);
-            if (live) {
-                v = make_float2(r.x, r.y);
-                if (blu) v = cmul(v, make_float2(r.z, r.w));
-            }
-            buf[__mul24(i, S) + sg] = v;
-        });
+    if (blu) {
+        seq_phase<NT, 4>(
+            M, lg, [&](int i) { return make_float4_2(at32(cb, crow + i), at32(chb, i)); },
+            [&](int i, float4 r) {
+                buf[__mul24(i, S) + sg] = live ? cmul(make_float2(r.x, r.y), make_float2(r.z, r.w))
+                                               : make_float2(0.f, 0.f);
+            });
+    } else {
+        seq_phase<NT, 4>(
+            M, lg, [&](int i) { return at32(cb, crow + i); },
+            [&](int i, float2 v) { buf[__mul24(i, S) + sg] = live ? v : make_float2(0.f, 0.f); });
+    }
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
@@ -539,20 +553,25 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
     const float* w = wt + bd.off;
     float2* Wb = W + (long long)it.s0 * C + bd.off;
     struct OutIn { float2 ch; float w; };
-    seq_phase<NT, 4>(
-        M, lg,
-        [&](int i) {
-            int slot = i + bd.rot;
-            if (slot >= M) slot -= M;
-            return OutIn{at32(chb, blu ? slot : 0), at32(w, i)};
-        },
-        [&](int i, const OutIn& r) {
-            int slot = i + bd.rot;
-            if (slot >= M) slot -= M;
-            float2 u = buf[__mul24(slot, S) + sg];
-            if (blu) u = cmul(r.ch, conjf2(u));
-            at32(Wb, crow + i) = cscale(u, r.w);
-        });
+    auto weigh = [&](auto blu_t) {
+        constexpr bool BLU = decltype(blu_t)::value;
+        seq_phase<NT, 4>(
+            M, lg,
+            [&](int i) {
+                int slot = i + bd.rot;
+                if (slot >= M) slot -= M;
+                return OutIn{BLU ? at32(chb, slot) : make_float2(1.f, 0.f), at32(w, i)};
+            },
+            [&](int i, const OutIn& r) {
+                int slot = i + bd.rot;
+                if (slot >= M) slot -= M;
+                float2 u = buf[__mul24(slot, S) + sg];
+                if (BLU) u = cmul(r.ch, conjf2(u));
+                at32(Wb, crow + i) = cscale(u, r.w);
+            });
+    };
+    if (blu) weigh(std::true_type{});
+    else weigh(std::false_type{});
 }
 
 // ------------------------------------------------------------ huge bands
