@@ -422,7 +422,7 @@ __device__ __forceinline__ void blu_middle(float2* buf, int n, int lg, int S, in
 // cyclic chirp exp(+i pi t^2/M), |t| < M.
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2* __restrict__ Z, float2* __restrict__ coef,
-                                                              const float* __restrict__ wt, Tables T, int item0,
+                                                              const float4* __restrict__ rt, Tables T, int item0,
                                                               int nitems, int batch, int L, long long C) {
     extern __shared__ float2 lds[];
     const WorkItem it = T.items[item0 + blockIdx.x];
@@ -441,10 +441,10 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
     const float2* Zb = Z + (long long)it.s0 * L;
     const uint32_t zrow = static_cast<uint32_t>(live ? sg : 0) * static_cast<uint32_t>(L);
     const float2* chb = T.chirp + (blu ? bd.chirp : 0);   // entry 0 is valid in every table
-    const float* w = wt + bd.off;
+    const float4* rb = rt + bd.off;
     // the chirp is read only by Bluestein bands (a uniform branch around
     // two instances of each phase)
-    struct RouteIn { float2 za, zb, om, ch; float w; };
+    struct RouteIn { float2 za, zb, ch; float4 r; };
     auto route = [&](auto blu_t) {
         constexpr bool BLU = decltype(blu_t)::value;
         seq_phase<NT, 4>(
@@ -455,19 +455,18 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                 const int k = bd.k_lo + i;
                 const int a = (k == L) ? 0 : k;
                 const int bm = (a == 0) ? 0 : L - a;
-                return RouteIn{at32(Zb, zrow + a), at32(Zb, zrow + bm), at32(T.omega, k),
-                               BLU ? at32(chb, slot) : make_float2(1.f, 0.f), at32(w, i)};
+                return RouteIn{at32(Zb, zrow + a), at32(Zb, zrow + bm),
+                               BLU ? at32(chb, slot) : make_float2(1.f, 0.f), at32(rb, i)};
             },
             [&](int i, const RouteIn& r) {
                 int slot = i + bd.rot;
                 if (slot >= M) slot -= M;
                 float2 v = make_float2(0.f, 0.f);
                 if (live) {
-                    const float2 pa = make_float2(1.f + r.om.y, -r.om.x);    // 1 - i w_k
-                    const float2 pb = make_float2(1.f - r.om.y, r.om.x);     // 1 + i w_k
-                    const float2 u2 = cadd(cmul(pa, r.za), cmul(pb, conjf2(r.zb)));
-                    const float hw = 0.5f * r.w;
-                    v = make_float2(hw * u2.x, -hw * u2.y);                  // conj(u)
+                    // u = (1/2) w (1 - i w_k) Z_a + (1/2) w (1 + i w_k) conj(Z_b)
+                    const float2 u = cadd(cmul(make_float2(r.r.x, r.r.y), r.za),
+                                          cmul(make_float2(r.r.z, r.r.w), conjf2(r.zb)));
+                    v = conjf2(u);
                     if (BLU) v = cmul(v, r.ch);
                 }
                 buf[__mul24(slot, S) + sg] = v;
@@ -588,7 +587,8 @@ struct BigArgs {
     float2* W;              // synthesis output (weighted band spectra), [b][C]
     float2* H1;             // four-step intermediate, [b][Hn]
     float2* H2;             // Bluestein first-FFT output, [b][Hn]
-    const float* wt;        // per-coefficient weights of the op
+    const float4* rt;       // analysis: router factors of the op
+    const float* wt;        // synthesis: per-coefficient weights of the op
     int L;
     long long C, Hn;
     int analysis;
@@ -636,12 +636,8 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
                     const int ka = (k == a.L) ? 0 : k;
                     const int kb = (ka == 0) ? 0 : a.L - ka;
                     const float2 za = Zs[ka], zb = Zs[kb];
-                    const float2 om = T.omega[k];
-                    const float2 pa = make_float2(1.f + om.y, -om.x);
-                    const float2 pb = make_float2(1.f - om.y, om.x);
-                    const float2 u2 = cadd(cmul(pa, za), cmul(pb, conjf2(zb)));
-                    const float hw = 0.5f * a.wt[bd.off + i];
-                    v = make_float2(hw * u2.x, -hw * u2.y);          // conj(u)
+                    const float4 r = a.rt[bd.off + i];             // router factors
+                    v = conjf2(cadd(cmul(make_float2(r.x, r.y), za), cmul(make_float2(r.z, r.w), conjf2(zb))));
                 } else {
                     v = a.cin[(long long)it.sig * a.C + bd.off + j];
                 }

@@ -46,6 +46,8 @@ struct nsgcqt_plan_s {
     const float* wS = nullptr;
     const float* wT = nullptr;
     const float* wSa = nullptr;
+    const float4* rA = nullptr;    // router factors of T and S^dagger
+    const float4* rSa = nullptr;
     std::vector<hipEvent_t> events;
     int ev_next = 0;
     std::map<const void*, int> resident;   // persistent kernels: workgroups resident at once
@@ -83,6 +85,8 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iWS = add(h.wS.data(), h.wS.size() * sizeof(float));
     const size_t iWT = add(h.wT.data(), h.wT.size() * sizeof(float));
     const size_t iWSa = add(h.wSa.data(), h.wSa.size() * sizeof(float));
+    const size_t iRA = add(h.rA.data(), h.rA.size() * sizeof(float));
+    const size_t iRSa = add(h.rSa.data(), h.rSa.size() * sizeof(float));
 
     char* d = nullptr;
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&d), total);
@@ -112,6 +116,8 @@ int upload(nsgcqt_plan_s* p) {
     p->wS = static_cast<const float*>(at(iWS));
     p->wT = static_cast<const float*>(at(iWT));
     p->wSa = static_cast<const float*>(at(iWSa));
+    p->rA = static_cast<const float4*>(at(iRA));
+    p->rSa = static_cast<const float4*>(at(iRSa));
     p->device = true;
     return NSGCQT_OK;
 }
@@ -267,8 +273,9 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
 }
 
 // The band tiers, one launch each.
-int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float* wt, int batch,
-              hipStream_t s) {
+// Analysis reads the router factors rt, synthesis the weights wt.
+int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float4* rt, const float* wt,
+              int batch, hipStream_t s) {
     const HostPlan& h = p->h;
     for (const auto& bk : h.buckets) {
         const int lds = bk.lds_elems * static_cast<int>(sizeof(float2));
@@ -277,7 +284,7 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
             ev_start(p, s);
             if (analysis) {
                 if (int r = launch_prep(ka, lds)) return r;
-                hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
+                hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, rt, p->T, bk.item_off, bk.nitems, batch,
                                    static_cast<int>(h.L), static_cast<long long>(h.C));
             } else {
                 if (int r = launch_prep(ks, lds)) return r;
@@ -337,18 +344,18 @@ BigArgs big_args(nsgcqt_plan_s* p, char* ws, int64_t hoff, int batch, bool analy
 }
 
 // Analysis chain (T, or S^dagger with its weights) for `batch` signals or slices.
-int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float* wt, int batch, SliceIn sl,
+int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float4* rt, int batch, SliceIn sl,
                   char* ws, hipStream_t s) {
     const HostPlan& h = p->h;
     float2* Y = reinterpret_cast<float2*>(ws);
     float2* Z = reinterpret_cast<float2*>(ws + align256(8 * h.L * batch));
     if (int r = run_fwd_a(p, x, Y, batch, sl, static_cast<long long>(h.N), s)) return r;
     if (int r = run_pass_b<false>(p, Y, Z, batch, static_cast<long long>(h.L), s)) return r;
-    if (int r = run_bands(p, true, Z, coeffs, wt, batch, s)) return r;
+    if (int r = run_bands(p, true, Z, coeffs, rt, nullptr, batch, s)) return r;
     BigArgs a = big_args(p, ws, h.off_h_an, h.spc ? h.spc : batch, true);
     a.Z = Z;
     a.cout = coeffs;
-    a.wt = wt;
+    a.rt = rt;
     return run_big(p, a, batch, s);
 }
 
@@ -358,7 +365,7 @@ int chain_synthesise(nsgcqt_plan_s* p, const float2* coeffs, float* xo, const fl
     const HostPlan& h = p->h;
     float2* W = reinterpret_cast<float2*>(ws);
     float2* Y = reinterpret_cast<float2*>(ws + align256(8 * h.C * batch));
-    if (int r = run_bands(p, false, coeffs, W, wt, batch, s)) return r;
+    if (int r = run_bands(p, false, coeffs, W, nullptr, wt, batch, s)) return r;
     BigArgs a = big_args(p, ws, h.off_h_syn, h.spc ? h.spc : batch, false);
     a.cin = coeffs;
     a.W = W;
@@ -506,7 +513,7 @@ int nsgcqt_plan_weights(nsgcqt_plan p, int which, float* dst, size_t bytes) {
 int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_t ws_bytes, void* stream) {
     if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, false)) return r;
     p->ev_next = 0;
-    return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->wA, p->h.batch, SliceIn{0, 0, 0, 0},
+    return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->rA, p->h.batch, SliceIn{0, 0, 0, 0},
                          static_cast<char*>(ws), static_cast<hipStream_t>(stream));
 }
 
@@ -527,7 +534,7 @@ int nsgcqt_adjoint(nsgcqt_plan p, int op, const float* in, float* out, void* ws,
     if (ta)
         return chain_synthesise(p, reinterpret_cast<const float2*>(in), out, p->wT, p->h.batch,
                                 static_cast<char*>(ws), s);
-    return chain_analyse(p, in, reinterpret_cast<float2*>(out), p->wSa, p->h.batch, SliceIn{0, 0, 0, 0},
+    return chain_analyse(p, in, reinterpret_cast<float2*>(out), p->rSa, p->h.batch, SliceIn{0, 0, 0, 0},
                          static_cast<char*>(ws), s);
 }
 
@@ -550,7 +557,7 @@ int nsgcqt_sliced_analyse(nsgcqt_plan p, const float* x, int64_t n, float* coeff
         const int cnt = static_cast<int>(std::min<int64_t>(h.spc, J - s0));
         SliceIn sl{1, static_cast<int>(s0), static_cast<long long>(n), static_cast<int>(h.N / 2)};
         float2* c = reinterpret_cast<float2*>(coeffs) + s0 * h.C;
-        if (int r = chain_analyse(p, x, c, p->wA, cnt, sl, static_cast<char*>(ws), s)) return r;
+        if (int r = chain_analyse(p, x, c, p->rA, cnt, sl, static_cast<char*>(ws), s)) return r;
     }
     return NSGCQT_OK;
 }

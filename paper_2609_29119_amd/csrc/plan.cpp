@@ -387,6 +387,24 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             p.wT[b.off + i] = static_cast<float>(static_cast<double>(N) / (d * M) * b.g[i]);
             p.wSa[b.off + i] = static_cast<float>(M * d / static_cast<double>(N) * b.h[i]);
         }
+    // router factors (eq. 7) in fp64, rounded once
+    p.rA.resize(4 * p.C); p.rSa.resize(4 * p.C);
+    for (auto& b : p.bands)
+        for (int64_t i = 0; i < b.M; ++i) {
+            const int64_t k = b.k_lo + i;
+            const double d = (k == 0 || k == half) ? 1.0 : 2.0;
+            const cd w = root(k, N), iw = cd(0.0, 1.0) * w;
+            const double wts[2] = {b.g[i], static_cast<double>(b.M) * d / static_cast<double>(N) * b.h[i]};
+            std::vector<float>* dst[2] = {&p.rA, &p.rSa};
+            for (int t = 0; t < 2; ++t) {
+                const cd pa = 0.5 * wts[t] * (1.0 - iw), pb = 0.5 * wts[t] * (1.0 + iw);
+                float* o = dst[t]->data() + 4 * (b.off + i);
+                o[0] = static_cast<float>(pa.real());
+                o[1] = static_cast<float>(pa.imag());
+                o[2] = static_cast<float>(pb.real());
+                o[3] = static_cast<float>(pb.imag());
+            }
+        }
 
     // ---- bin ownership for the overlap-add and fan-out statistics
     p.owner.assign(half + 1, -1);

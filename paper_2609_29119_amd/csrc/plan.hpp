@@ -58,6 +58,10 @@ struct HostPlan {
 
     // fp32 tables
     std::vector<float> wA, wS, wT, wSa;     // C each, bin order
+    // router factors of the analysis chains (T with g, S^dagger with its
+    // weight w): (1/2) w (1 - i w_k) and (1/2) w (1 + i w_k) per coefficient,
+    // as 4 floats (re, im, re, im), bin order
+    std::vector<float> rA, rSa;
     std::vector<FftDesc> ffts;
     std::vector<float> twpool;              // interleaved complex
     std::vector<float> omega;               // exp(-2 pi i k / N), k = 0..L
