@@ -33,7 +33,7 @@ struct Tables {
     const float2* omega;     // exp(-2 pi i k / N), k = 0..L
     const int32_t* owner;    // first band covering bin k | count << 24, k = 0..L
     const int32_t* bandbase; // off - k_lo per band
-    const int4* gather;      // per bin k = 0..L: W indices of up to 3 covering bands, count
+    const int4* gather;      // per bin k = 0..L: covering bands of k and of L - k (head, steps) x 2
     const float2* chirp;     // Bluestein exp(-i pi m^2 / M)
     const float2* kern;      // Bluestein DFT_P(b) / P
     const float2* tw4_hi;
@@ -208,15 +208,20 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_fwd_a(const float* __restrict__ 
     }
 }
 
-// X_q = sum of the weighted band spectra W over the (at most three) bands
-// covering bin q; the bin's record holds their W indices (unused ones 0, a
-// valid index) and count. All three reads are issued unconditionally.
 __device__ __forceinline__ float4 make_float4_2(float2 a, float2 b) { return make_float4(a.x, a.y, b.x, b.y); }
 
-__device__ __forceinline__ float2 gather_bin(const float2* __restrict__ Ws, int4 g) {
-    const float2 a = at32(Ws, g.x), b = at32(Ws, g.y), c = at32(Ws, g.z);
+// X_q = sum of the weighted band spectra W over the (at most three) bands
+// covering bin q. The bin's half-record `head` holds the first band's W
+// index with the count in bits 29..31, `steps` the int16 steps to the second
+// and third bands' indices (0 where absent, so every index stays valid). All
+// three reads are issued unconditionally.
+__device__ __forceinline__ float2 gather_bin(const float2* __restrict__ Ws, int head, int steps) {
+    const int i0 = head & ((1 << 29) - 1), cnt = static_cast<int>(static_cast<unsigned>(head) >> 29);
+    const int i1 = i0 + static_cast<int>(static_cast<short>(steps & 0xFFFF));
+    const int i2 = i1 + (steps >> 16);
+    const float2 a = at32(Ws, i0), b = at32(Ws, i1), c = at32(Ws, i2);
     // masks instead of branches, so the compiler cannot sink the reads
-    const float mb = g.w > 1 ? 1.f : 0.f, mc = g.w > 2 ? 1.f : 0.f;
+    const float mb = cnt > 1 ? 1.f : 0.f, mc = cnt > 2 ? 1.f : 0.f;
     return make_float2(a.x + mb * b.x + mc * c.x, a.y + mb * b.y + mc * c.y);
 }
 
@@ -257,26 +262,25 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     const int ncols = min(H, (pair ? (p.L2 >> 1) + 1 : p.L2) - c0);  // primary columns here
     const int tot = p.L1 << lgH;
     const float2* Ws = W + (long long)sig * C;
-    // U elements at a time: the bin records of q and L - q and the twiddle of
-    // q, then the W values they name, then the retangles; indices are clamped
+    // U elements at a time: the bin record (of q and L - q) and the twiddle of
+    // q, then the W values it names, then the retangles; indices are clamped
     // into the tile
     constexpr int U = 4;
     for (int base = threadIdx.x; base < tot; base += U * NT) {
-        int4 gq[U], gm[U];
+        int4 g[U];
         float2 oq[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int e = min(base + u * NT, tot - 1);
             const int q = __mul24(e >> lgH, p.L2) + c0 + min(e & (H - 1), ncols - 1);
-            gq[u] = at32(T.gather, q);
-            gm[u] = at32(T.gather, p.L - q);
+            g[u] = at32(T.gather, q);      // bins q and L - q
             oq[u] = at32(T.omega, q);
         }
         float2 xq[U], xm[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            xq[u] = gather_bin(Ws, gq[u]);
-            xm[u] = gather_bin(Ws, gm[u]);
+            xq[u] = gather_bin(Ws, g[u].x, g[u].y);
+            xm[u] = gather_bin(Ws, g[u].z, g[u].w);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {

@@ -67,7 +67,7 @@ struct HostPlan {
     std::vector<float> omega;               // exp(-2 pi i k / N), k = 0..L
     std::vector<float> tw4_hi, tw4_lo;      // four-step twiddles
     std::vector<int32_t> owner;             // per bin k = 0..L: first band | count << 24
-    std::vector<int32_t> gather;            // per bin k = 0..L: W index of up to 3 covering bands, count
+    std::vector<int32_t> gather;            // per bin k = 0..L: covering bands of k and of L - k (see plan.cpp)
     std::vector<int32_t> bandbase;          // per band: off - k_lo
     std::vector<BandDev> banddev;
     std::vector<float> chirp, kern;         // Bluestein tables
