@@ -25,6 +25,13 @@ notes of the repository):
     centre bin k_c = floor(xi + 1/2) (0 for DC, N/2 for Nyquist);
   * bands with empty support are dropped.
 
+An explicit band list (``build_band_layout``) uses the same window shapes at
+given centres and widths with lengths M >= the support width: the slots past
+the support hold zero, which is the band spectrum zero-padded to M (Sec. 2
+only asks that E_lambda place the support injectively into M slots).
+``table1_specs`` is the multi-resolution layout of Table 1 (Sec. 4) under the
+reading stated in its docstring.
+
 Parity: pinned by tests (closed-form windows, sum h g = 1, coverage bounds,
 band counts, agreement with an independent integer layout).
 """
@@ -50,10 +57,15 @@ class Band:
     g: np.ndarray = None  # window on k_lo..k_hi (fp64)
     h: np.ndarray = None  # dual window on k_lo..k_hi (fp64)
     offset: int = 0       # first coefficient of this band in the flat layout
+    length: int = 0       # band length M; 0 means the support width
+
+    @property
+    def width(self) -> int:
+        return self.k_hi - self.k_lo + 1
 
     @property
     def M(self) -> int:
-        return self.k_hi - self.k_lo + 1
+        return self.length or self.width
 
     @property
     def bins(self) -> np.ndarray:
@@ -137,6 +149,12 @@ def build_layout(fs, fmin, fmax, bins_per_octave, N) -> Layout:
     g = np.where(k >= xl + bl, 1.0, np.sin(np.pi * (k - xl) / (2.0 * bl)) ** 2)
     bands.append(Band(NYQUIST, k_lo, half, half, xl, bl, fs / 2.0, g))
 
+    a = _finish(bands, half)
+    return Layout(float(fs), float(fmin), float(fmax), B, N, bands, a)
+
+
+def _finish(bands, half):
+    """Offsets, aggregate weight a_k = sum M g^2 and duals h = M g / a (Sec. 2)."""
     a = np.zeros(half + 1)
     off = 0
     for band in bands:
@@ -147,4 +165,85 @@ def build_layout(fs, fmin, fmax, bins_per_octave, N) -> Layout:
         raise ValueError("layout leaves a bin uncovered (a_k = 0)")
     for band in bands:
         band.h = band.M * band.g / a[band.k_lo:band.k_hi + 1]
-    return Layout(float(fs), float(fmin), float(fmax), B, N, bands, a)
+    return a
+
+
+def build_band_layout(fs, N, specs) -> Layout:
+    """Layout of an explicit band list: tuples (kind, xi, beta, length[, centre_hz]).
+
+    DC: bins 0 <= k < xi, flat up to xi - beta, then sin^2(pi (xi - k)/(2 beta)).
+    POSITIVE: Hann cos^2(pi (k - xi)/(2 beta)) on |k - xi| < beta within 0..N/2,
+    centre bin floor(xi + 1/2). NYQUIST: bins xi < k <= N/2, sin^2(pi (k - xi)/(2 beta))
+    below xi + beta, then flat. length 0 means the support width; otherwise it
+    must be at least the support width."""
+    N = int(N)
+    if N % 2 or N < 4:
+        raise ValueError("N must be even and >= 4")
+    half = N // 2
+    bands = []
+    for i, sp in enumerate(specs):
+        kind, xi, beta, length = int(sp[0]), float(sp[1]), float(sp[2]), int(sp[3])
+        f = float(sp[4]) if len(sp) > 4 else 0.0
+        if not (beta > 0.0 and math.isfinite(xi) and math.isfinite(beta)) or length < 0:
+            raise ValueError(f"band {i}: invalid width or length")
+        if kind == DC:
+            if i != 0:
+                raise ValueError("a DC band must come first")
+            k = np.arange(0, min(half, math.ceil(xi) - 1) + 1)
+            g = np.where(k <= xi - beta, 1.0, np.sin(np.pi * (xi - k) / (2.0 * beta)) ** 2)
+            k_c = 0
+        elif kind == POSITIVE:
+            k = np.arange(max(0, math.floor(xi - beta) + 1), min(half, math.ceil(xi + beta) - 1) + 1)
+            g = _hann(k, xi, beta)
+            k_c = math.floor(xi + 0.5)
+        elif kind == NYQUIST:
+            if i != len(specs) - 1:
+                raise ValueError("a Nyquist band must come last")
+            k = np.arange(max(0, math.floor(xi) + 1), half + 1)
+            g = np.where(k >= xi + beta, 1.0, np.sin(np.pi * (k - xi) / (2.0 * beta)) ** 2)
+            k_c = half
+        else:
+            raise ValueError(f"band {i}: unknown kind")
+        if len(k) == 0:
+            raise ValueError(f"band {i}: empty support")
+        if length and length < len(k):
+            raise ValueError(f"band {i}: length below the support width")
+        bands.append(Band(kind, int(k[0]), int(k[-1]), k_c, xi, beta, f, g, length=length))
+    a = _finish(bands, half)
+    return Layout(float(fs), 0.0, 0.0, 0, N, bands, a)
+
+
+def table1_specs():
+    """(fs, N, band list) of the multi-resolution layout of Table 1 (Sec. 4).
+
+    The paper fixes N = 65,536 at 44.1 kHz, three resolutions covering 3, 4
+    and 2 octaves at 8, 16 and 32 bands per octave (152 positive bands),
+    centres rounded to bins with the highest adjusted towards Nyquist, one
+    length per octave from its widest support rounded up to a power of two,
+    and sideband lengths 128 (DC) and 2048 (Nyquist). Reading of what it
+    leaves open: the lowest centre is bin 64 (43.07 Hz, the table's 43 Hz);
+    centre j of octave o (o = 0..8) is bin round(64 * 2^(o + j/B_o)); the
+    highest centre is the table's 21,810 Hz rounded to a bin; each window is
+    the Hann window of the constant-Q reading with Q = 1/(2^(1/B_o) - 1) and
+    half-amplitude width xi/Q; the sidebands complement the outer halves of
+    the lowest and highest windows."""
+    fs, N = 44100.0, 65536
+    half = N // 2
+    per_octave = [8] * 3 + [16] * 4 + [32] * 2
+    octave, xis = [], []
+    for o, B in enumerate(per_octave):
+        for j in range(B):
+            octave.append(o)
+            xis.append(float(round(64.0 * 2.0 ** (o + j / B))))
+    xis[-1] = float(round(21810.0 * N / fs))
+    betas = [xi / (1.0 / (2.0 ** (1.0 / per_octave[o]) - 1.0)) for xi, o in zip(xis, octave)]
+    widest = [0] * len(per_octave)
+    for xi, beta, o in zip(xis, betas, octave):
+        lo = max(0, math.floor(xi - beta) + 1)
+        hi = min(half, math.ceil(xi + beta) - 1)
+        widest[o] = max(widest[o], hi - lo + 1)
+    length = [1 << (w - 1).bit_length() for w in widest]
+    specs = [(DC, xis[0], betas[0], 128, 0.0)]
+    specs += [(POSITIVE, xi, beta, length[o], xi * fs / N) for xi, beta, o in zip(xis, betas, octave)]
+    specs.append((NYQUIST, xis[-1], betas[-1], 2048, fs / 2.0))
+    return fs, N, specs

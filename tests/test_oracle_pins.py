@@ -304,6 +304,115 @@ def test_property_reconstruction_and_adjoints(N, B, fmin_frac, fmax_frac):
     np.testing.assert_allclose(hg, 1.0, atol=1e-12)
 
 
+# --------------------------------------------------------- explicit band lists
+
+def test_table1_layout_pins():
+    # Table 1 and Sec. 4: N = 65,536 at 44.1 kHz, 152 positive bands (8, 8, 8,
+    # 16, 16, 16, 16, 32, 32 per octave) plus DC and Nyquist sidebands of
+    # lengths 128 and 2048, one length per octave (32 ... 2048) obtained by
+    # rounding the octave's widest support up to a power of two, and 132,992
+    # coefficients per slice. The lengths here come from that rounding rule
+    # applied to the reading's window widths, so they pin the widths.
+    fs, N, specs = oracle.table1_specs()
+    assert (fs, N) == (44100.0, 65536)
+    lay = oracle.build_band_layout(fs, N, specs)
+    kinds = [b.kind for b in lay.bands]
+    assert kinds == [DC] + [POSITIVE] * 152 + [NYQUIST]
+    lengths = [b.M for b in lay.bands[1:-1]]
+    table = [(8, 32), (8, 64), (8, 128), (16, 128), (16, 256), (16, 512), (16, 1024), (32, 1024), (32, 2048)]
+    assert lengths == [M for n, M in table for _ in range(n)]
+    assert (lay.bands[0].M, lay.bands[-1].M) == (128, 2048)
+    assert lay.n_coeffs == 132992
+    # painless: every support fits its length; every bin covered
+    assert all(b.width <= b.M for b in lay.bands)
+    assert np.all(lay.a > 0)
+    # centres: the table's lowest (43 Hz) and highest (21,810 Hz) to a bin,
+    # and each octave's printed range to within 7 % (the spacing inside the
+    # resolutions is not stated)
+    hz = [b.centre_hz for b in lay.bands[1:-1]]
+    assert abs(hz[0] - 43.0) < 44100 / 65536 and abs(hz[-1] - 21810.0) < 44100 / 65536
+    ranges = [(43, 81), (88, 165), (180, 337), (345, 666), (695, 1342), (1402, 2708), (2830, 5464),
+              (5512, 10905), (11147, 21810)]
+    i = 0
+    for (n, _), (lo, hi) in zip(table, ranges):
+        oc = hz[i:i + n]
+        i += n
+        assert abs(oc[0] / lo - 1) < 0.07 and abs(oc[-1] / hi - 1) < 0.07
+    hg = np.zeros(lay.half + 1)
+    for b in lay.bands:
+        hg[b.k_lo:b.k_hi + 1] += b.h * b.g
+    np.testing.assert_allclose(hg, 1.0, atol=1e-12)
+
+
+def _padded_specs(N):
+    # a small band list with lengths above the support widths, sidebands included
+    half = N // 2
+    xs = [3.0, 5.5, 8.0, 11.0, 14.5, 18.0]
+    specs = [(DC, xs[0], 2.0, 7)]
+    specs += [(POSITIVE, x, 3.1, L) for x, L in zip(xs, [0, 9, 8, 13, 8, 11])]
+    specs.append((NYQUIST, xs[-1], 3.1, half - 14))
+    return specs
+
+
+def test_padded_band_list_brute_force():
+    N = 40
+    lay = oracle.build_band_layout(40.0, N, _padded_specs(N))
+    assert any(b.M > b.width for b in lay.bands)
+    T = _analysis_matrix_by_sums(lay)
+    I = np.eye(N)
+    np.testing.assert_allclose(oracle.analyse(lay, I).T, T, atol=1e-12)
+    np.testing.assert_allclose(oracle.synthesise(lay, oracle.analyse(lay, I)), I, atol=1e-12)
+    rng = np.random.default_rng(3)
+    y = rng.standard_normal(T.shape[0]) + 1j * rng.standard_normal(T.shape[0])
+    np.testing.assert_allclose(oracle.adjoint_analysis(lay, y), np.real(np.conj(T).T @ y), atol=1e-12)
+    x = rng.standard_normal(N)
+    lhs = np.sum(oracle.synthesise(lay, y) * x)
+    rhs = np.sum(np.real(np.conj(y) * oracle.adjoint_synthesis(lay, x)))
+    assert lhs == pytest.approx(rhs, rel=1e-12)
+
+
+def test_zero_padding_doubles_time_resolution():
+    # A band spectrum zero-padded from M to 2M slots, frequencies d = k - k_c
+    # kept, gives c'[2n] = c[n] / 2: (1/2M) sum u_d e^{2 pi i d 2n / 2M}.
+    N = 256
+    base = [(DC, 6.0, 3.0, 0)] + [(POSITIVE, 6.0 * 1.5 ** j, 1.5 ** j * 3.0, 0) for j in range(7)]
+    base.append((NYQUIST, base[-1][1], base[-1][2], 0))
+    lay1 = oracle.build_band_layout(256.0, N, base)
+    double = [(k, xi, be, 2 * b.M) for (k, xi, be, _), b in zip(base, lay1.bands)]
+    lay2 = oracle.build_band_layout(256.0, N, double)
+    x = np.random.default_rng(9).standard_normal(N)
+    c1 = oracle.split_bands(lay1, oracle.analyse(lay1, x))
+    c2 = oracle.split_bands(lay2, oracle.analyse(lay2, x))
+    for a, b in zip(c1, c2):
+        np.testing.assert_allclose(b[0::2], a / 2, atol=1e-13)
+    # both are frames of the same signal
+    assert oracle.snr_db(x, oracle.synthesise(lay2, oracle.analyse(lay2, x))) > 250
+
+
+def test_table1_reconstruction_and_adjoint():
+    fs, N, specs = oracle.table1_specs()
+    lay = oracle.build_band_layout(fs, N, specs)
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal(N)
+    c = oracle.analyse(lay, x, mode="fft")
+    assert oracle.snr_db(x, oracle.synthesise(lay, c, mode="fft")) > 250
+    y = rng.standard_normal(lay.n_coeffs) + 1j * rng.standard_normal(lay.n_coeffs)
+    lhs = np.sum(np.real(np.conj(c) * y))
+    rhs = np.sum(x * oracle.adjoint_analysis(lay, y, mode="fft"))
+    assert lhs == pytest.approx(rhs, rel=1e-11)
+
+
+def test_band_list_rejections():
+    N = 40
+    good = _padded_specs(N)
+    with pytest.raises(ValueError):          # length below the support width
+        oracle.build_band_layout(40.0, N, [good[0], (POSITIVE, 8.0, 3.1, 4)] + good[2:])
+    with pytest.raises(ValueError):          # DC not first
+        oracle.build_band_layout(40.0, N, good[1:2] + good[0:1] + good[2:])
+    with pytest.raises(ValueError):          # uncovered bins
+        oracle.build_band_layout(40.0, N, good[:2])
+
+
 # ---------------------------------------------------------------- sliced mode
 
 def test_slice_window_partition_of_unity():
