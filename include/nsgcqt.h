@@ -32,6 +32,11 @@
  *     halves, M = support width, the centre bin in slot 0. Dual windows are
  *     h = M g / a with a_k = sum M g^2 (Sec. 2). Bands with empty support
  *     are dropped at plan time.
+ *   - Plans may instead take an explicit band list (nsgcqt_plan_create_bands):
+ *     the same window shapes at given centres and widths, with lengths M at
+ *     least the support width. Slots of a band past its support hold zero
+ *     in analysis and are ignored by synthesis, as zero-padding the band
+ *     spectrum to M (Sec. 2: E_lambda places the support injectively).
  *
  * Pointers and ownership
  *   - x, coeffs, outputs and the workspace are device pointers owned by the
@@ -84,7 +89,7 @@ typedef struct {
     int64_t k_lo;       /* first support bin */
     int64_t k_hi;       /* last support bin (inclusive) */
     int64_t k_centre;   /* bin placed in slot 0: slot(k) = (k - k_centre) mod M */
-    int64_t length;     /* M = k_hi - k_lo + 1 */
+    int64_t length;     /* M >= k_hi - k_lo + 1 (equal for constant-Q plans) */
     int64_t offset;     /* first coefficient of the band in a row of C */
     double centre_hz;   /* 0 for DC, fs/2 for Nyquist */
     double xi;          /* centre in bins (unrounded) of the governing Hann window */
@@ -94,6 +99,25 @@ typedef struct {
     int64_t bluestein;  /* 1 if the band uses Bluestein's algorithm (two
                            length-P transforms), 0 otherwise; independent of batch */
 } nsgcqt_band;
+
+/* One band of an explicit layout (Sec. 2: window g, selection E, length M).
+ * All widths and centres are in bins of the length-N DFT.
+ *   NSGCQT_BAND_POSITIVE: Hann window g(k) = cos^2(pi (k - xi) / (2 beta)) on
+ *       the bins with |k - xi| < beta, clipped to 0 <= k <= N/2; the bin
+ *       floor(xi + 1/2) goes to slot 0.
+ *   NSGCQT_BAND_DC: bins 0 <= k < xi, g = 1 for k <= xi - beta and
+ *       sin^2(pi (xi - k) / (2 beta)) above (the complement of the lower half
+ *       of a Hann window at xi, beta); bin 0 in slot 0. First band only.
+ *   NSGCQT_BAND_NYQUIST: bins xi < k <= N/2, g = sin^2(pi (k - xi) / (2 beta))
+ *       below xi + beta and 1 from there; bin N/2 in slot 0. Last band only.
+ * slot(k) = (k - k_centre) mod length. length 0 means the support width. */
+typedef struct {
+    int32_t kind;       /* nsgcqt_band_kind */
+    double xi;          /* centre in bins (sidebands: the neighbouring Hann's centre) */
+    double beta;        /* half-amplitude width in bins, > 0 */
+    int64_t length;     /* M >= support width, or 0 for the support width */
+    double centre_hz;   /* reported by nsgcqt_band_info only */
+} nsgcqt_band_spec;
 
 typedef struct {
     int64_t n_bands;          /* bands kept */
@@ -148,6 +172,38 @@ int nsgcqt_sliced_plan_create(nsgcqt_plan* out, double fs, double fmin, double f
 /* Host-only variant of nsgcqt_sliced_plan_create. */
 int nsgcqt_sliced_plan_create_host(nsgcqt_plan* out, double fs, double fmin, double fmax,
                                    int bins_per_octave, int64_t slice_len, int slices_per_chunk);
+
+/* Plan of an explicit band list bands[0 .. n_bands-1] (nsgcqt_band_spec)
+ * for `batch` signals of n_samples real samples at sample rate fs; the band
+ * order is the coefficient order. Bands covering one bin must be adjacent in
+ * the list (ascending centres satisfy this). Windows, dual windows and
+ * every table follow exactly as for nsgcqt_plan_create.
+ * EINVAL: out or bands NULL, n_bands < 1, N odd or < 4, fs <= 0, batch < 1,
+ *         a kind other than 0..2, a DC band that is not first or a Nyquist
+ *         band that is not last, xi not finite, beta not finite or <= 0,
+ *         length < 0, a band with empty support, a length below the support
+ *         width, or a bin no band covers (a_k = 0).
+ * EUNSUPPORTED: as for nsgcqt_plan_create, and for bands covering one bin
+ *         that are not adjacent, more than three bands on one bin, or a
+ *         length of 2^28 or more. */
+int nsgcqt_plan_create_bands(nsgcqt_plan* out, double fs, int64_t n_samples, int batch,
+                             int n_bands, const nsgcqt_band_spec* bands);
+
+/* Host-only variant of nsgcqt_plan_create_bands. */
+int nsgcqt_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t n_samples, int batch,
+                                  int n_bands, const nsgcqt_band_spec* bands);
+
+/* The multi-resolution layout of Table 1 (Sec. 4): N = 65,536 at 44.1 kHz;
+ * octaves 1-3 at 8, 4-7 at 16 and 8-9 at 32 bands per octave above a lowest
+ * centre of 64 bins (43.07 Hz), centres rounded to bins and the highest one
+ * at 21,810 Hz; each octave's bands share the length of its widest support
+ * rounded up to a power of two; DC and Nyquist sidebands of lengths 128 and
+ * 2048 (154 bands, C = 132,992). Writes the band count to *n_bands and, when
+ * not NULL, the sample rate and length to *fs and *n_samples; with out
+ * non-NULL also the bands, which need capacity >= *n_bands (EINVAL
+ * otherwise). Pass the result to nsgcqt_plan_create_bands. */
+int nsgcqt_layout_table1(nsgcqt_band_spec* out, int capacity, int* n_bands, double* fs,
+                         int64_t* n_samples);
 
 /* Free the plan and its device tables. Any work using it must have
  * completed. NULL is accepted. */

@@ -415,8 +415,8 @@ __device__ __forceinline__ void blu_middle(float2* buf, int n, int lg, int S, in
 }
 
 // One workgroup per work item (band, signals s0 .. s0 + count - 1, interleaved
-// as 2^lgnb sequences). For entry i of the band (bin k = k_lo + i) the router
-// (eq. 7) forms
+// as 2^lgnb sequences). For entry i < W of the band (bin k = k_lo + i; slots
+// of entries W <= i < M, past the support, hold zero) the router (eq. 7) forms
 //   u = (1/2) w [(1 - i w_k) Z_{k mod L} + (1 + i w_k) conj(Z_{-k mod L})]
 // with w the band's weight at k (g for T, the S^dagger weight for S^dagger),
 // places conj(u) at slot (k - k_c) mod M in LDS, and the band's inverse DFT
@@ -456,7 +456,8 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
             [&](int i) {
                 int slot = i + bd.rot;
                 if (slot >= M) slot -= M;
-                const int k = bd.k_lo + i;
+                // entries past the support read a valid bin; their factors are zero
+                const int k = bd.k_lo + min(i, bd.W - 1);
                 const int a = (k == L) ? 0 : k;
                 const int bm = (a == 0) ? 0 : L - a;
                 return RouteIn{at32(Zb, zrow + a), at32(Zb, zrow + bm),
@@ -466,7 +467,7 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                 int slot = i + bd.rot;
                 if (slot >= M) slot -= M;
                 float2 v = make_float2(0.f, 0.f);
-                if (live) {
+                if (live && i < bd.W) {
                     // u = (1/2) w (1 - i w_k) Z_a + (1/2) w (1 + i w_k) conj(Z_b)
                     const float2 u = cadd(cmul(make_float2(r.r.x, r.r.y), r.za),
                                           cmul(make_float2(r.r.z, r.r.w), conjf2(r.zb)));
@@ -508,8 +509,8 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
 
 // ----------------------------------------------------------- band synthesis
 // One workgroup per work item: U = F_M c (eq. 10), then the weighted band
-// spectrum W[off + i] = w_i U[slot(k_lo + i)] in bin order (w = h for S, the
-// T^dagger weight for T^dagger). Overlapping bands are summed later by the
+// spectrum W[off + i] = w_i U[slot(k_lo + i)] in bin order for the support
+// entries i < W (w = h for S, the T^dagger weight for T^dagger). Overlapping bands are summed later by the
 // owner of each bin.
 template <int NT, int EPT>
 __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2* __restrict__ coef, float2* __restrict__ W,
@@ -559,7 +560,7 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
     auto weigh = [&](auto blu_t) {
         constexpr bool BLU = decltype(blu_t)::value;
         seq_phase<NT, 4>(
-            M, lg,
+            bd.W, lg,
             [&](int i) {
                 int slot = i + bd.rot;
                 if (slot >= M) slot -= M;
@@ -635,13 +636,15 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
                 if (in_mode == kBigInRoute) {
                     int i = j - bd.rot;
                     if (i < 0) i += M;
-                    const int k = bd.k_lo + i;
-                    const float2* Zs = a.Z + (long long)it.sig * a.L;
-                    const int ka = (k == a.L) ? 0 : k;
-                    const int kb = (ka == 0) ? 0 : a.L - ka;
-                    const float2 za = Zs[ka], zb = Zs[kb];
-                    const float4 r = a.rt[bd.off + i];             // router factors
-                    v = conjf2(cadd(cmul(make_float2(r.x, r.y), za), cmul(make_float2(r.z, r.w), conjf2(zb))));
+                    if (i < bd.W) {   // slots past the support hold zero
+                        const int k = bd.k_lo + i;
+                        const float2* Zs = a.Z + (long long)it.sig * a.L;
+                        const int ka = (k == a.L) ? 0 : k;
+                        const int kb = (ka == 0) ? 0 : a.L - ka;
+                        const float2 za = Zs[ka], zb = Zs[kb];
+                        const float4 r = a.rt[bd.off + i];             // router factors
+                        v = conjf2(cadd(cmul(make_float2(r.x, r.y), za), cmul(make_float2(r.z, r.w), conjf2(zb))));
+                    }
                 } else {
                     v = a.cin[(long long)it.sig * a.C + bd.off + j];
                 }
@@ -707,7 +710,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_b(BigArgs a, Tables T, int i
                 const float2 u = blu ? cmul(T.chirp[bd.chirp + k], conjf2(v)) : v;
                 int i = k - bd.rot;
                 if (i < 0) i += M;
-                a.W[(long long)it.sig * a.C + bd.off + i] = cscale(u, a.wt[bd.off + i]);
+                if (i < bd.W) a.W[(long long)it.sig * a.C + bd.off + i] = cscale(u, a.wt[bd.off + i]);
             }
         }
     }

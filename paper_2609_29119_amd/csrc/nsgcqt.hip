@@ -389,8 +389,10 @@ int check_call(nsgcqt_plan_s* p, const void* in, const void* out, const void* ws
     return NSGCQT_OK;
 }
 
-int create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t n, int batch, bool sliced,
-           bool device) {
+// Builds the host plan with `build(HostPlan&, std::string& err)` and, for a
+// device plan, uploads its tables.
+template <class Build>
+int create(nsgcqt_plan* out, bool device, Build build) {
     if (!out) return set_err(NSGCQT_EINVAL, "out is NULL");
     *out = nullptr;
     nsgcqt_plan_s* p = new (std::nothrow) nsgcqt_plan_s();
@@ -398,7 +400,7 @@ int create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64
     std::string err;
     int r;
     try {
-        r = build_host_plan(p->h, fs, fmin, fmax, bpo, n, batch, sliced, err);
+        r = build(p->h, err);
     } catch (const std::bad_alloc&) {
         r = NSGCQT_ENOMEM;
         err = "host allocation failed while building the plan";
@@ -423,27 +425,74 @@ int create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64
     return NSGCQT_OK;
 }
 
+auto cq_builder(double fs, double fmin, double fmax, int bpo, int64_t n, int batch, bool sliced) {
+    return [=](HostPlan& h, std::string& err) { return build_host_plan(h, fs, fmin, fmax, bpo, n, batch, sliced, err); };
+}
+
+int create_bands(nsgcqt_plan* out, double fs, int64_t n, int batch, int n_bands, const nsgcqt_band_spec* bands,
+                 bool device) {
+    if (out) *out = nullptr;
+    if (n_bands < 1) return set_err(NSGCQT_EINVAL, "n_bands must be >= 1");
+    if (!bands) return set_err(NSGCQT_EINVAL, "bands is NULL");
+    std::vector<BandSpec> specs(n_bands);
+    for (int i = 0; i < n_bands; ++i)
+        specs[i] = BandSpec{bands[i].kind, bands[i].xi, bands[i].beta, bands[i].length, bands[i].centre_hz};
+    return create(out, device, [&](HostPlan& h, std::string& err) {
+        return build_host_plan_bands(h, fs, n, batch, specs, err);
+    });
+}
+
 }  // namespace
 
 extern "C" {
 
 int nsgcqt_plan_create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t n, int batch) {
-    return create(out, fs, fmin, fmax, bpo, n, batch, false, true);
+    return create(out, true, cq_builder(fs, fmin, fmax, bpo, n, batch, false));
 }
 
 int nsgcqt_plan_create_host(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t n,
                             int batch) {
-    return create(out, fs, fmin, fmax, bpo, n, batch, false, false);
+    return create(out, false, cq_builder(fs, fmin, fmax, bpo, n, batch, false));
 }
 
 int nsgcqt_sliced_plan_create(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo, int64_t slice_len,
                               int spc) {
-    return create(out, fs, fmin, fmax, bpo, slice_len, spc, true, true);
+    return create(out, true, cq_builder(fs, fmin, fmax, bpo, slice_len, spc, true));
 }
 
 int nsgcqt_sliced_plan_create_host(nsgcqt_plan* out, double fs, double fmin, double fmax, int bpo,
                                    int64_t slice_len, int spc) {
-    return create(out, fs, fmin, fmax, bpo, slice_len, spc, true, false);
+    return create(out, false, cq_builder(fs, fmin, fmax, bpo, slice_len, spc, true));
+}
+
+int nsgcqt_plan_create_bands(nsgcqt_plan* out, double fs, int64_t n_samples, int batch, int n_bands,
+                             const nsgcqt_band_spec* bands) {
+    return create_bands(out, fs, n_samples, batch, n_bands, bands, true);
+}
+
+int nsgcqt_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t n_samples, int batch, int n_bands,
+                                  const nsgcqt_band_spec* bands) {
+    return create_bands(out, fs, n_samples, batch, n_bands, bands, false);
+}
+
+int nsgcqt_layout_table1(nsgcqt_band_spec* out, int capacity, int* n_bands, double* fs, int64_t* n_samples) {
+    if (!n_bands) return set_err(NSGCQT_EINVAL, "n_bands is NULL");
+    std::vector<BandSpec> specs;
+    table1_specs(specs);
+    *n_bands = static_cast<int>(specs.size());
+    if (fs) *fs = kTable1Fs;
+    if (n_samples) *n_samples = kTable1N;
+    if (!out) return NSGCQT_OK;
+    if (capacity < static_cast<int>(specs.size()))
+        return set_err(NSGCQT_EINVAL, "capacity below the " + std::to_string(specs.size()) + " bands of the layout");
+    for (size_t i = 0; i < specs.size(); ++i) {
+        out[i].kind = specs[i].kind;
+        out[i].xi = specs[i].xi;
+        out[i].beta = specs[i].beta;
+        out[i].length = specs[i].M;
+        out[i].centre_hz = specs[i].f;
+    }
+    return NSGCQT_OK;
 }
 
 int nsgcqt_plan_destroy(nsgcqt_plan p) {

@@ -281,15 +281,13 @@ int64_t bluestein_length(int64_t M, int64_t row_bytes, double* cost) {
 
 }  // namespace
 
-int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
-                    int64_t N, int batch, bool sliced, std::string& err) {
+namespace {
+
+// Checks and settings shared by both plan builders.
+int begin_plan(HostPlan& p, double fs, int64_t N, int batch, bool sliced, std::string& err) {
     if (!(N >= 4) || (N % 2) != 0)
         return fail(err, NSGCQT_EINVAL, "n_samples must be even and >= 4");
     if (!(fs > 0.0)) return fail(err, NSGCQT_EINVAL, "fs must be > 0");
-    if (!(fmin > 0.0) || !(fmin < fs / 2.0))
-        return fail(err, NSGCQT_EINVAL, "fmin must satisfy 0 < fmin < fs/2");
-    if (!(fmax >= fmin)) return fail(err, NSGCQT_EINVAL, "fmax must be >= fmin");
-    if (B < 1) return fail(err, NSGCQT_EINVAL, "bins_per_octave must be >= 1");
     if (batch < 1) return fail(err, NSGCQT_EINVAL, "batch must be >= 1");
     if (sliced && (N % 8) != 0)
         return fail(err, NSGCQT_EINVAL, "slice length must be a multiple of 8");
@@ -297,11 +295,26 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     // with 32-bit byte offsets
     if (N >= (int64_t(1) << 29))
         return fail(err, NSGCQT_EUNSUPPORTED, "n_samples of 2^29 or more");
-
-    p.fs = fs; p.fmin = fmin; p.fmax = fmax; p.bpo = B;
+    p.fs = fs;
     p.N = N; p.L = N / 2; p.batch = batch; p.sliced = sliced;
     p.spc = sliced ? batch : 0;
-    const int64_t half = N / 2, L = p.L;
+    p.bands.clear();
+    return NSGCQT_OK;
+}
+
+int finish_plan(HostPlan& p, std::string& err);
+
+}  // namespace
+
+int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
+                    int64_t N, int batch, bool sliced, std::string& err) {
+    if (int r = begin_plan(p, fs, N, batch, sliced, err)) return r;
+    if (!(fmin > 0.0) || !(fmin < fs / 2.0))
+        return fail(err, NSGCQT_EINVAL, "fmin must satisfy 0 < fmin < fs/2");
+    if (!(fmax >= fmin)) return fail(err, NSGCQT_EINVAL, "fmax must be >= fmin");
+    if (B < 1) return fail(err, NSGCQT_EINVAL, "bins_per_octave must be >= 1");
+    p.fmin = fmin; p.fmax = fmax; p.bpo = B;
+    const int64_t half = N / 2;
 
     // ---- layout: geometric centres, Hann windows, DC and Nyquist sidebands
     const double Q = 1.0 / (std::pow(2.0, 1.0 / B) - 1.0);
@@ -313,7 +326,6 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         xis.push_back(f * static_cast<double>(N) / fs);
         betas.push_back((f / Q) * static_cast<double>(N) / fs);
     }
-    p.bands.clear();
     {
         const double xi0 = xis.front(), b0 = betas.front();
         HostBand b{};
@@ -353,17 +365,132 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         }
         p.bands.push_back(std::move(b));
     }
+    // constant-Q bands are as long as their support
+    for (auto& b : p.bands) b.M = b.width();
+    return finish_plan(p, err);
+}
+
+int build_host_plan_bands(HostPlan& p, double fs, int64_t N, int batch, const std::vector<BandSpec>& specs,
+                          std::string& err) {
+    if (int r = begin_plan(p, fs, N, batch, false, err)) return r;
+    p.fmin = 0.0; p.fmax = 0.0; p.bpo = 0;
+    if (specs.empty()) return fail(err, NSGCQT_EINVAL, "the band list is empty");
+    if (specs.size() >= (size_t(1) << 24)) return fail(err, NSGCQT_EUNSUPPORTED, "too many bands");
+    const int64_t half = N / 2;
+    for (size_t i = 0; i < specs.size(); ++i) {
+        const BandSpec& s = specs[i];
+        const std::string name = "band " + std::to_string(i);
+        if (s.kind < 0 || s.kind > 2) return fail(err, NSGCQT_EINVAL, name + ": kind must be 0, 1 or 2");
+        if (s.kind == 0 && i != 0) return fail(err, NSGCQT_EINVAL, name + ": a DC band must come first");
+        if (s.kind == 2 && i + 1 != specs.size()) return fail(err, NSGCQT_EINVAL, name + ": a Nyquist band must come last");
+        if (!std::isfinite(s.xi) || !(s.beta > 0.0) || !std::isfinite(s.beta) || std::fabs(s.xi) > 1e15 || s.beta > 1e15)
+            return fail(err, NSGCQT_EINVAL, name + ": xi must be finite and beta finite and > 0");
+        if (s.M < 0) return fail(err, NSGCQT_EINVAL, name + ": length must be >= 0");
+        HostBand b{};
+        b.kind = s.kind; b.xi = s.xi; b.beta = s.beta; b.f = s.f;
+        if (s.kind == 0) {
+            // flat, then a sin^2 taper complementing the lower half of the Hann window at xi
+            b.k_lo = 0;
+            b.k_hi = std::min<int64_t>(half, static_cast<int64_t>(std::ceil(s.xi)) - 1);
+            b.k_c = 0;
+            for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+                const double kd = static_cast<double>(k);
+                const double sn = std::sin(kPi * (s.xi - kd) / (2.0 * s.beta));
+                b.g.push_back(kd <= s.xi - s.beta ? 1.0 : sn * sn);
+            }
+        } else if (s.kind == 1) {
+            b.k_lo = std::max<int64_t>(0, static_cast<int64_t>(std::floor(s.xi - s.beta)) + 1);
+            b.k_hi = std::min<int64_t>(half, static_cast<int64_t>(std::ceil(s.xi + s.beta)) - 1);
+            b.k_c = static_cast<int64_t>(std::floor(s.xi + 0.5));
+            for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+                const double c = std::cos(kPi * (static_cast<double>(k) - s.xi) / (2.0 * s.beta));
+                b.g.push_back(c * c);
+            }
+        } else {
+            // a sin^2 taper complementing the upper half of the Hann window at xi, then flat
+            b.k_lo = std::max<int64_t>(0, static_cast<int64_t>(std::floor(s.xi)) + 1);
+            b.k_hi = half;
+            b.k_c = half;
+            for (int64_t k = b.k_lo; k <= b.k_hi; ++k) {
+                const double kd = static_cast<double>(k);
+                const double sn = std::sin(kPi * (kd - s.xi) / (2.0 * s.beta));
+                b.g.push_back(kd >= s.xi + s.beta ? 1.0 : sn * sn);
+            }
+        }
+        if (b.k_hi < b.k_lo) return fail(err, NSGCQT_EINVAL, name + ": empty support");
+        b.M = s.M ? s.M : b.width();
+        if (b.M < b.width())
+            return fail(err, NSGCQT_EINVAL, name + ": length " + std::to_string(b.M) + " below its support width " +
+                                                std::to_string(b.width()));
+        if (b.M >= (int64_t(1) << 28)) return fail(err, NSGCQT_EUNSUPPORTED, name + ": length of 2^28 or more");
+        p.bands.push_back(std::move(b));
+    }
+    return finish_plan(p, err);
+}
+
+void table1_specs(std::vector<BandSpec>& out) {
+    // Nine octaves above a lowest centre of 64 bins (43.07 Hz): octaves 1-3
+    // at 8, 4-7 at 16 and 8-9 at 32 bands per octave. Centre j of octave o
+    // is 64 * 2^(o + j/B) bins (o from 0), rounded to a bin; the highest
+    // centre is the table's 21,810 Hz, rounded to a bin. Each Hann window
+    // has half-amplitude width xi/Q with Q = 1/(2^(1/B) - 1) of its octave.
+    // Every band of an octave has the length of the octave's widest
+    // support, rounded up to a power of two; the DC and Nyquist sidebands
+    // have lengths 128 and 2048.
+    static const int kBpo[9] = {8, 8, 8, 16, 16, 16, 16, 32, 32};
+    const double N = static_cast<double>(kTable1N), fs = kTable1Fs;
+    const int64_t half = kTable1N / 2;
+    out.clear();
+    std::vector<BandSpec> pos;
+    std::vector<int> oct;
+    for (int o = 0; o < 9; ++o) {
+        const int B = kBpo[o];
+        for (int j = 0; j < B; ++j) {
+            BandSpec s{};
+            s.kind = 1;
+            s.xi = std::nearbyint(64.0 * std::pow(2.0, o + static_cast<double>(j) / B));
+            pos.push_back(s);
+            oct.push_back(o);
+        }
+    }
+    pos.back().xi = std::nearbyint(21810.0 * N / fs);
+    for (size_t i = 0; i < pos.size(); ++i) {
+        const double Q = 1.0 / (std::pow(2.0, 1.0 / kBpo[oct[i]]) - 1.0);
+        pos[i].beta = pos[i].xi / Q;
+        pos[i].f = pos[i].xi * fs / N;
+    }
+    int64_t widest[9] = {0};
+    for (size_t i = 0; i < pos.size(); ++i) {
+        const int64_t lo = std::max<int64_t>(0, static_cast<int64_t>(std::floor(pos[i].xi - pos[i].beta)) + 1);
+        const int64_t hi = std::min<int64_t>(half, static_cast<int64_t>(std::ceil(pos[i].xi + pos[i].beta)) - 1);
+        widest[oct[i]] = std::max(widest[oct[i]], hi - lo + 1);
+    }
+    for (size_t i = 0; i < pos.size(); ++i) {
+        int64_t M = 1;
+        while (M < widest[oct[i]]) M *= 2;
+        pos[i].M = M;
+    }
+    out.push_back(BandSpec{0, pos.front().xi, pos.front().beta, 128, 0.0});
+    out.insert(out.end(), pos.begin(), pos.end());
+    out.push_back(BandSpec{2, pos.back().xi, pos.back().beta, 2048, fs / 2.0});
+}
+
+namespace {
+
+int finish_plan(HostPlan& p, std::string& err) {
+    const int64_t N = p.N, L = p.L, half = N / 2;
+    const int batch = p.batch;
+    const bool sliced = p.sliced;
 
     // ---- aggregate weight and dual windows (Sec. 2)
     p.a.assign(half + 1, 0.0);
     int64_t off = 0;
     p.maxM = 0;
     for (auto& b : p.bands) {
-        b.M = b.k_hi - b.k_lo + 1;
         b.off = off;
         off += b.M;
         p.maxM = std::max(p.maxM, b.M);
-        for (int64_t i = 0; i < b.M; ++i) p.a[b.k_lo + i] += static_cast<double>(b.M) * b.g[i] * b.g[i];
+        for (int64_t i = 0; i < b.width(); ++i) p.a[b.k_lo + i] += static_cast<double>(b.M) * b.g[i] * b.g[i];
     }
     p.C = off;
     for (int64_t k = 0; k <= half; ++k)
@@ -371,14 +498,15 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     if (p.C * static_cast<int64_t>(batch) * 8 > (int64_t(1) << 46))
         return fail(err, NSGCQT_EUNSUPPORTED, "coefficient array too large");
     for (auto& b : p.bands) {
-        b.h.resize(b.M);
-        for (int64_t i = 0; i < b.M; ++i) b.h[i] = static_cast<double>(b.M) * b.g[i] / p.a[b.k_lo + i];
+        b.h.resize(b.width());
+        for (int64_t i = 0; i < b.width(); ++i) b.h[i] = static_cast<double>(b.M) * b.g[i] / p.a[b.k_lo + i];
     }
 
-    // ---- per-coefficient weight tables in bin order (Sec. 3, eq. 7 and Sec. 3.2)
-    p.wA.resize(p.C); p.wS.resize(p.C); p.wT.resize(p.C); p.wSa.resize(p.C);
+    // ---- per-coefficient weight tables in bin order (Sec. 3, eq. 7 and Sec. 3.2);
+    // the entries of a band past its support are zero
+    p.wA.assign(p.C, 0.f); p.wS.assign(p.C, 0.f); p.wT.assign(p.C, 0.f); p.wSa.assign(p.C, 0.f);
     for (auto& b : p.bands)
-        for (int64_t i = 0; i < b.M; ++i) {
+        for (int64_t i = 0; i < b.width(); ++i) {
             const int64_t k = b.k_lo + i;
             const double d = (k == 0 || k == half) ? 1.0 : 2.0;
             const double M = static_cast<double>(b.M);
@@ -388,9 +516,9 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
             p.wSa[b.off + i] = static_cast<float>(M * d / static_cast<double>(N) * b.h[i]);
         }
     // router factors (eq. 7) in fp64, rounded once
-    p.rA.resize(4 * p.C); p.rSa.resize(4 * p.C);
+    p.rA.assign(4 * p.C, 0.f); p.rSa.assign(4 * p.C, 0.f);
     for (auto& b : p.bands)
-        for (int64_t i = 0; i < b.M; ++i) {
+        for (int64_t i = 0; i < b.width(); ++i) {
             const int64_t k = b.k_lo + i;
             const double d = (k == 0 || k == half) ? 1.0 : 2.0;
             const cd w = root(k, N), iw = cd(0.0, 1.0) * w;
@@ -539,6 +667,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
         BandDev d{};
         d.k_lo = static_cast<int32_t>(b.k_lo);
         d.M = static_cast<int32_t>(b.M);
+        d.W = static_cast<int32_t>(b.width());
         d.rot = static_cast<int32_t>(((b.k_lo - b.k_c) % b.M + b.M) % b.M);
         d.off = static_cast<int32_t>(b.off);
         d.inv_M = static_cast<float>(1.0 / static_cast<double>(b.M));
@@ -707,5 +836,7 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
     if (sliced) p.ws_syn += align256(4 * N * b) + 2 * align256(4 * (N / 2));
     return NSGCQT_OK;
 }
+
+}  // namespace
 
 }  // namespace nsg

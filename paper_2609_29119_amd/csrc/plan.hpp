@@ -12,9 +12,24 @@ namespace nsg {
 
 struct HostBand {
     int kind;             // 0 DC, 1 positive, 2 Nyquist
-    int64_t k_lo, k_hi, k_c, M, off;
+    int64_t k_lo, k_hi, k_c;
+    int64_t M;            // band length (transform length), at least the support width
+    int64_t off;
     double f, xi, beta;
     std::vector<double> g, h;   // on k_lo..k_hi
+    int64_t width() const { return k_hi - k_lo + 1; }
+};
+
+// One band of an explicit layout: the window kind (0 DC, 1 positive,
+// 2 Nyquist), the centre xi and half-amplitude width beta (in bins) of the
+// band's Hann window (for a sideband, of the neighbouring Hann window whose
+// outer half it complements), and the band length M (0: the support width).
+// f is the centre in Hz, reported only.
+struct BandSpec {
+    int kind;
+    double xi, beta;
+    int64_t M;
+    double f;
 };
 
 // Band kernels are launched per bucket; each bucket has one thread count and
@@ -94,6 +109,15 @@ struct HostPlan {
 // Returns 0 on success, or a negative nsgcqt status with `err` set.
 int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int bpo,
                     int64_t N, int batch, bool sliced, std::string& err);
+
+// Plan of an explicit band list (see BandSpec); same return convention.
+int build_host_plan_bands(HostPlan& p, double fs, int64_t N, int batch, const std::vector<BandSpec>& specs,
+                          std::string& err);
+
+// The multi-resolution layout of the paper's Table 1 (N = 65,536 at 44.1 kHz).
+constexpr int64_t kTable1N = 65536;
+constexpr double kTable1Fs = 44100.0;
+void table1_specs(std::vector<BandSpec>& out);
 
 // Radix factorisation used by the Stockham stages: primes above 16 (at most
 // max_prime) become stages of their own, the remaining factors are packed

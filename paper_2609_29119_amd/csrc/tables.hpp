@@ -51,7 +51,8 @@ struct FftDesc {
 // One band of the layout as the band kernels see it.
 struct BandDev {
     int32_t k_lo;      // first support bin
-    int32_t M;         // band length = support width
+    int32_t M;         // band length, at least the support width
+    int32_t W;         // support width: entries i < W hold bins k_lo + i
     int32_t rot;       // slot of bin k_lo: (k_lo - k_c) mod M
     int32_t off;       // first coefficient of the band in a row
     int32_t fft;       // FftDesc index: length M, or P for Bluestein

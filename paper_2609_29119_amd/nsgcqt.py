@@ -27,7 +27,8 @@ EXPORTS = [
     "nsgcqt_band_info", "nsgcqt_plan_weights", "nsgcqt_analyse", "nsgcqt_synthesise",
     "nsgcqt_adjoint", "nsgcqt_sliced_count", "nsgcqt_sliced_analyse",
     "nsgcqt_sliced_synthesise", "nsgcqt_set_stage_events", "nsgcqt_stage_info",
-    "nsgcqt_last_error",
+    "nsgcqt_last_error", "nsgcqt_plan_create_bands", "nsgcqt_plan_create_bands_host",
+    "nsgcqt_layout_table1",
 ]
 
 
@@ -49,6 +50,16 @@ class BandInfo(ctypes.Structure):
                 ("k_centre", ctypes.c_int64), ("length", ctypes.c_int64), ("offset", ctypes.c_int64),
                 ("centre_hz", ctypes.c_double), ("xi", ctypes.c_double), ("beta", ctypes.c_double),
                 ("fft_len", ctypes.c_int64), ("bluestein", ctypes.c_int64)]
+
+
+class BandSpec(ctypes.Structure):
+    """One band of an explicit layout: kind, centre xi and half-width beta in
+    bins, length M (0: the support width), centre in Hz (reported only)."""
+    _fields_ = [("kind", ctypes.c_int32), ("xi", ctypes.c_double), ("beta", ctypes.c_double),
+                ("length", ctypes.c_int64), ("centre_hz", ctypes.c_double)]
+
+    def as_tuple(self):
+        return (int(self.kind), float(self.xi), float(self.beta), int(self.length), float(self.centre_hz))
 
 
 _lib = None
@@ -82,6 +93,10 @@ def lib():
         "nsgcqt_set_stage_events": [P, ctypes.POINTER(ctypes.c_void_p), I],
         "nsgcqt_stage_info": [P, I, I, ctypes.c_char_p, ctypes.c_size_t, ctypes.POINTER(ctypes.c_double)],
         "nsgcqt_last_error": [],
+        "nsgcqt_plan_create_bands": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
+        "nsgcqt_plan_create_bands_host": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
+        "nsgcqt_layout_table1": [ctypes.POINTER(BandSpec), I, ctypes.POINTER(ctypes.c_int),
+                                 ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -117,15 +132,21 @@ class Plan:
     (streaming) plan. device=False builds the host tables only.
     """
 
-    def __init__(self, fs, fmin, fmax, bins_per_octave, n_samples, batch=1, device=True, _sliced=False):
+    def __init__(self, fs, fmin, fmax, bins_per_octave, n_samples, batch=1, device=True, _sliced=False,
+                 _bands=None):
         L = lib()
         h = ctypes.c_void_p()
-        if _sliced:
-            fn = L.nsgcqt_sliced_plan_create if device else L.nsgcqt_sliced_plan_create_host
+        if _bands is not None:
+            arr = (BandSpec * len(_bands))(*[BandSpec(*b) for b in _bands])
+            fn = L.nsgcqt_plan_create_bands if device else L.nsgcqt_plan_create_bands_host
+            _check(fn(ctypes.byref(h), float(fs), int(n_samples), int(batch), len(_bands), arr))
         else:
-            fn = L.nsgcqt_plan_create if device else L.nsgcqt_plan_create_host
-        _check(fn(ctypes.byref(h), float(fs), float(fmin), float(fmax), int(bins_per_octave),
-                  int(n_samples), int(batch)))
+            if _sliced:
+                fn = L.nsgcqt_sliced_plan_create if device else L.nsgcqt_sliced_plan_create_host
+            else:
+                fn = L.nsgcqt_plan_create if device else L.nsgcqt_plan_create_host
+            _check(fn(ctypes.byref(h), float(fs), float(fmin), float(fmax), int(bins_per_octave),
+                      int(n_samples), int(batch)))
         self._h = h
         self.info = Info()
         _check(L.nsgcqt_plan_info(self._h, ctypes.byref(self.info)))
@@ -135,6 +156,12 @@ class Plan:
     @classmethod
     def sliced(cls, fs, fmin, fmax, bins_per_octave, slice_len, slices_per_chunk=16, device=True):
         return cls(fs, fmin, fmax, bins_per_octave, slice_len, slices_per_chunk, device, _sliced=True)
+
+    @classmethod
+    def from_bands(cls, fs, n_samples, bands, batch=1, device=True):
+        """Plan of an explicit band list: tuples (kind, xi, beta, length[, centre_hz])
+        as nsgcqt_band_spec, in coefficient order."""
+        return cls(fs, 0.0, 0.0, 0, n_samples, batch, device, _bands=[tuple(b) for b in bands])
 
     def close(self):
         if getattr(self, "_h", None):
@@ -295,3 +322,15 @@ class Plan:
         if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or not t.is_cuda:
             raise ValueError(f"expected a contiguous cuda {dtype} tensor of shape {tuple(shape)}, "
                              f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def table1_layout():
+    """The Table-1 multi-resolution layout: (fs, n_samples, band tuples)."""
+    L = lib()
+    n = ctypes.c_int()
+    fs = ctypes.c_double()
+    N = ctypes.c_int64()
+    _check(L.nsgcqt_layout_table1(None, 0, ctypes.byref(n), ctypes.byref(fs), ctypes.byref(N)))
+    arr = (BandSpec * n.value)()
+    _check(L.nsgcqt_layout_table1(arr, n.value, ctypes.byref(n), None, None))
+    return fs.value, N.value, [b.as_tuple() for b in arr]

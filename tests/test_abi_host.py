@@ -98,7 +98,8 @@ def _packed_eval(p, lay, x):
     for b in p.bands():
         k = np.arange(b.k_lo, b.k_hi + 1)
         a = k % L
-        u = 0.5 * g[b.offset:b.offset + b.length] * ((1 - 1j * om[k]) * Z[a] + (1 + 1j * om[k]) * np.conj(Z[(-a) % L]))
+        W = b.k_hi - b.k_lo + 1                # support width (<= length)
+        u = 0.5 * g[b.offset:b.offset + W] * ((1 - 1j * om[k]) * Z[a] + (1 + 1j * om[k]) * np.conj(Z[(-a) % L]))
         v = np.zeros(b.length, complex)
         v[(k - b.k_centre) % b.length] = u     # eq. 7 router, then eq. 8
         c[b.offset:b.offset + b.length] = np.fft.ifft(v)
@@ -106,7 +107,7 @@ def _packed_eval(p, lay, x):
     for b in p.bands():
         k = np.arange(b.k_lo, b.k_hi + 1)
         U = np.fft.fft(c[b.offset:b.offset + b.length])
-        X[k] += hw[b.offset:b.offset + b.length] * U[(k - b.k_centre) % b.length]
+        X[k] += hw[b.offset:b.offset + len(k)] * U[(k - b.k_centre) % b.length]
     X[0], X[L] = X[0].real, X[L].real
     q = np.arange(L)
     Zs = 0.5 * ((1 + 1j * np.conj(om[q])) * X[q] + (1 - 1j * np.conj(om[q])) * np.conj(X[L - q]))   # eq. 9
@@ -251,3 +252,101 @@ def test_compute_calls_reject_bad_arguments(lib):
     assert lib.nsgcqt_band_info(h, p.n_bands, ctypes.byref(nb.BandInfo())) == nb.EINVAL
     assert lib.nsgcqt_plan_weights(h, 9, buf, 1 << 20) == nb.EINVAL
     assert lib.nsgcqt_plan_destroy(None) == nb.OK
+
+
+# ------------------------------------------------------ explicit band lists
+
+def test_table1_preset_identical_to_oracle(lib):
+    fs, N, specs = nb.table1_layout()
+    ofs, oN, ospecs = oracle.table1_specs()
+    assert (fs, N) == (ofs, oN)
+    assert [tuple(b) for b in specs] == [tuple(b) for b in ospecs]
+    p = nb.Plan.from_bands(fs, N, specs, batch=4, device=False)
+    lay = oracle.build_band_layout(fs, N, ospecs)
+    assert p.n_bands == 154 and p.n_coeffs == lay.n_coeffs == 132992
+    for i, (ob, cb) in enumerate(zip(lay.bands, p.bands())):
+        assert (cb.kind, cb.k_lo, cb.k_hi, cb.k_centre, cb.length, cb.offset) == \
+               (ob.kind, ob.k_lo, ob.k_hi, ob.k_c, ob.M, ob.offset), i
+    # power-of-two lengths: every band runs a direct transform
+    assert not any(b.bluestein for b in p.bands())
+    assert p.info.max_overlap == 3
+
+
+def _band_list_case():
+    # padded lengths, a length with a prime factor above 257 (Bluestein) and
+    # a Nyquist band longer than N / 2
+    N, fs = 1200, 1200.0
+    xs = [8.0 * 1.35 ** j for j in range(12)]
+    specs = [(nb.BAND_DC, xs[0], xs[0] * 0.35, 16)]
+    lens = [0, 8, 0, 20, 0, 31, 40, 0, 67, 0, 2 * 263, 160]
+    specs += [(nb.BAND_POSITIVE, x, x * 0.35, L, x) for x, L in zip(xs, lens)]
+    specs.append((nb.BAND_NYQUIST, xs[-1], xs[-1] * 0.35, 1500))
+    return fs, N, specs
+
+
+def test_band_list_layout_and_weights_match_oracle(lib):
+    fs, N, specs = _band_list_case()
+    lay = oracle.build_band_layout(fs, N, specs)
+    p = nb.Plan.from_bands(fs, N, specs, batch=2, device=False)
+    assert p.n_coeffs == lay.n_coeffs
+    for i, (ob, cb) in enumerate(zip(lay.bands, p.bands())):
+        assert (cb.kind, cb.k_lo, cb.k_hi, cb.k_centre, cb.length, cb.offset) == \
+               (ob.kind, ob.k_lo, ob.k_hi, ob.k_c, ob.M, ob.offset), i
+    assert any(b.bluestein for b in p.bands())
+    half = N // 2
+    ref = {w: np.zeros(lay.n_coeffs) for w in (nb.WEIGHT_G, nb.WEIGHT_H, nb.WEIGHT_ADJ_ANALYSIS,
+                                               nb.WEIGHT_ADJ_SYNTHESIS)}
+    for b in lay.bands:
+        k = b.bins
+        d = np.where((k == 0) | (k == half), 1.0, 2.0)
+        sl = slice(b.offset, b.offset + b.width)
+        ref[nb.WEIGHT_G][sl] = b.g
+        ref[nb.WEIGHT_H][sl] = b.h
+        ref[nb.WEIGHT_ADJ_ANALYSIS][sl] = N / (d * b.M) * b.g
+        ref[nb.WEIGHT_ADJ_SYNTHESIS][sl] = b.M * d / N * b.h
+    for which, r in ref.items():
+        np.testing.assert_allclose(p.weights(which).astype(np.float64), r, rtol=1e-7, atol=1e-30)
+    # the library's tables drive the packed path (eqs. 5-10) to the oracle
+    x = workloads.white(8, 1, N)[0].astype(np.float64)
+    c, xr = _packed_eval(p, lay, x)
+    assert oracle.rel_l2(c, oracle.analyse(lay, x)) < 3e-7
+    assert oracle.snr_db(x, xr) > 130.0
+
+
+def _spec_status(lib, fs, N, specs, batch=1):
+    arr = (nb.BandSpec * max(1, len(specs)))(*[nb.BandSpec(*b) for b in specs])
+    h = ctypes.c_void_p()
+    st = lib.nsgcqt_plan_create_bands_host(ctypes.byref(h), fs, N, batch, len(specs), arr)
+    if h.value:
+        lib.nsgcqt_plan_destroy(h)
+    return st, h
+
+
+def test_band_list_rejections(lib):
+    fs, N, specs = _band_list_case()
+    assert _spec_status(lib, fs, N, specs)[0] == nb.OK
+    bad = {
+        "length below width": specs[:3] + [(nb.BAND_POSITIVE, specs[3][1], specs[3][2], 2)] + specs[4:],
+        "DC not first": specs[1:2] + specs[0:1] + specs[2:],
+        "Nyquist not last": specs[:-2] + specs[-1:] + specs[-2:-1],
+        "beta <= 0": specs[:2] + [(nb.BAND_POSITIVE, specs[2][1], 0.0, 0)] + specs[3:],
+        "kind": specs[:2] + [(5, specs[2][1], specs[2][2], 0)] + specs[3:],
+        "empty support": specs[:2] + [(nb.BAND_POSITIVE, 10.5, 0.4, 0)] + specs[2:],
+        "uncovered": specs[:3],
+        "negative length": specs[:2] + [(nb.BAND_POSITIVE, specs[2][1], specs[2][2], -1)] + specs[3:],
+        "nan centre": specs[:2] + [(nb.BAND_POSITIVE, float("nan"), specs[2][2], 0)] + specs[3:],
+    }
+    for what, sp in bad.items():
+        st, h = _spec_status(lib, fs, N, sp)
+        assert st == nb.EINVAL and not h.value, what
+    assert _spec_status(lib, fs, N, [])[0] == nb.EINVAL
+    assert _spec_status(lib, fs, N + 1, specs)[0] == nb.EINVAL
+    assert _spec_status(lib, fs, N, specs, batch=0)[0] == nb.EINVAL
+    # bands covering one bin that are not adjacent in the list
+    swapped = specs[:4] + [specs[5], specs[4]] + specs[6:]
+    assert _spec_status(lib, fs, N, swapped)[0] == nb.EUNSUPPORTED
+    n = ctypes.c_int()
+    assert lib.nsgcqt_layout_table1(None, 0, None, None, None) == nb.EINVAL
+    assert lib.nsgcqt_layout_table1((nb.BandSpec * 10)(), 10, ctypes.byref(n), None, None) == nb.EINVAL
+    assert n.value == 154
+

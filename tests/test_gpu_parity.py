@@ -233,6 +233,67 @@ def test_huge_bands_small_layout():
     assert oracle.rel_l2(ta, oracle.adjoint_analysis(lay, y, mode="fft")).max() <= REL_TOL
 
 
+def _check_all_ops(p, lay, x, y, xs, mode="direct"):
+    c = p.analyse(to_gpu(x))
+    assert oracle.rel_l2(to_np(c), oracle.analyse(lay, x, mode=mode)).max() <= REL_TOL
+    assert oracle.snr_db(x, to_np(p.synthesise(c))).min() >= SNR_MIN
+    sy = to_np(p.synthesise(to_gpu(y)))
+    assert oracle.rel_l2(sy, oracle.synthesise(lay, y, mode=mode)).max() <= REL_TOL
+    ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
+    assert oracle.rel_l2(ta, oracle.adjoint_analysis(lay, y, mode=mode)).max() <= REL_TOL
+    sa = to_np(p.adjoint(nb.OP_ADJ_SYNTHESIS, to_gpu(xs)))
+    assert oracle.rel_l2(sa, oracle.adjoint_synthesis(lay, xs, mode=mode)).max() <= REL_TOL
+
+
+def test_table1_layout_against_oracle():
+    # the paper's Table-1 layout (N = 65,536, power-of-two band lengths above
+    # the supports) through an explicit band list
+    fs, N, specs = nb.table1_layout()
+    lay = oracle.build_band_layout(fs, N, specs)
+    b = 3
+    p = nb.Plan.from_bands(fs, N, specs, batch=b)
+    x = workloads.white(65536, b, N)
+    y = workloads.coeff_cotangent(65537, b, p.n_coeffs)
+    xs = workloads.signal_cotangent(65538, b, N)
+    _check_all_ops(p, lay, x, y, xs, mode="fft")
+    # one signal against the direct band DFTs
+    one = nb.Plan.from_bands(fs, N, specs, batch=1)
+    cg = to_np(one.analyse(to_gpu(x[:1])))
+    assert oracle.rel_l2(cg, oracle.analyse(lay, x[:1])).max() <= REL_TOL
+
+
+def _padded_list(N, xs, lens, rel=0.35, dc_len=0, ny_len=0):
+    specs = [(nb.BAND_DC, xs[0], xs[0] * rel, dc_len)]
+    specs += [(nb.BAND_POSITIVE, x, x * rel, L) for x, L in zip(xs, lens)]
+    specs.append((nb.BAND_NYQUIST, xs[-1], xs[-1] * rel, ny_len))
+    return specs
+
+
+BAND_LISTS = [
+    # padded lengths; prime factors 31 and 67 (matrix-core stages); 2 * 263
+    # (Bluestein); a Nyquist band longer than N / 2
+    ("padded_N1200", 1200, [8.0 * 1.35 ** j for j in range(12)],
+     [0, 8, 0, 20, 0, 31, 40, 0, 67, 0, 2 * 263, 160], 16, 1500, 2, "direct"),
+    # lengths beyond one workgroup: 8200 = 8 * 25 * 41 direct, 8209 (prime)
+    # Bluestein and a Nyquist band of 9000, all through the huge-band path
+    ("huge_N4000", 4000, [10.0 * 1.4 ** j for j in range(14)],
+     [0, 0, 0, 0, 0, 0, 8200, 0, 0, 8209, 0, 0, 0, 0], 0, 9000, 2, "fft"),
+]
+
+
+@pytest.mark.parametrize("case", BAND_LISTS, ids=[c[0] for c in BAND_LISTS])
+def test_band_list_against_oracle(case):
+    name, N, xs, lens, dc_len, ny_len, b, mode = case
+    specs = _padded_list(N, xs, lens, dc_len=dc_len, ny_len=ny_len)
+    lay = oracle.build_band_layout(float(N), N, specs)
+    p = nb.Plan.from_bands(float(N), N, specs, batch=b)
+    assert any(bd.length > bd.k_hi - bd.k_lo + 1 for bd in p.bands())
+    x = workloads.white(N + 5, b, N)
+    y = workloads.coeff_cotangent(N + 6, b, p.n_coeffs)
+    xs_ = workloads.signal_cotangent(N + 7, b, N)
+    _check_all_ops(p, lay, x, y, xs_, mode=mode)
+
+
 def test_workspace_too_small_raises():
     w = workloads.WORKLOADS["tiny"]
     p = nb.Plan(*w.plan_args, batch=1)
