@@ -6,7 +6,12 @@ of synthetic audio resident in HBM. Default workload: 128 signals of 88,200
 samples at 22.05 kHz, 55 Hz..fs/2 at 36 bins per octave (the throughput
 stress workload). Prints one JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--batch B]
+                  [--mode roundtrip|step]
+
+--mode step times the differentiable round trip of the paper's second
+experiment instead (eager: T, S, squared error against a target, and the
+backward pass through the explicit adjoints).
 """
 from __future__ import annotations
 
@@ -81,6 +86,21 @@ def traffic_from_profiles(workload, kernel):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
+def make_plan(w, batch):
+    import paper_2609_29119_amd as nc
+    if w.layout == "table1":
+        fs, N, specs = nc.table1_layout()
+        return nc.Plan.from_bands(fs, N, specs, batch=batch)
+    return nc.Plan(*w.plan_args, batch=batch)
+
+
+def describe(w, b, N):
+    if w.layout == "table1":
+        return f"{w.name}: {b} x {N} samples @ {w.fs:g} Hz, Table 1 multi-resolution layout (154 bands)"
+    return (f"{w.name}: {b} x {N} samples @ {w.fs:g} Hz, {w.fmin:g} Hz..fs/2, "
+            f"{w.bins_per_octave} bins/oct")
+
+
 def cpu_baseline(w, x, target_s=12.0):
     """The fp64 oracle's round trip (analysis + synthesis) timed on a bounded
     sample of the workload: signal counts double until one run reaches the
@@ -88,7 +108,10 @@ def cpu_baseline(w, x, target_s=12.0):
     about target_s seconds of CPU work have been timed in total."""
     import oracle
     from threadpoolctl import threadpool_info
-    lay = oracle.build_layout(*w.plan_args)
+    if w.layout == "table1":
+        lay = oracle.build_band_layout(*oracle.table1_specs())
+    else:
+        lay = oracle.build_layout(*w.plan_args)
     k = 1
     while True:
         t0 = time.perf_counter()
@@ -201,7 +224,10 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="stress")
+    ap.add_argument("--batch", type=int, default=0, help="signals per step (default: the workload's)")
+    ap.add_argument("--mode", choices=("roundtrip", "step"), default="roundtrip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
     ap.add_argument("--no-stage-events", action="store_true",
                     help="time the loop without per-kernel events (for profiler runs)")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
@@ -226,11 +252,14 @@ def main():
     w = workloads.WORKLOADS[args.workload]
     if w.slice_len:
         raise SystemExit("bench runs full-length workloads; use the sliced tests for the long one")
+    b = args.batch or w.batch
     torch.cuda.init()
-    plan = nc.Plan(*w.plan_args, batch=w.batch)
-    x_np = workloads.signals(w)
+    plan = make_plan(w, b)
+    x_np = workloads.signals(w, batch=b)
     x = torch.from_numpy(x_np).cuda()
-    c = torch.empty((w.batch, plan.n_coeffs), dtype=torch.complex64, device="cuda")
+    if args.mode == "step":
+        return bench_step(args, w, plan, x)
+    c = torch.empty((b, plan.n_coeffs), dtype=torch.complex64, device="cuda")
     xr = torch.empty_like(x)
     ws_a = plan.workspace(nc.OP_ANALYSE)
     ws_s = plan.workspace(nc.OP_SYNTHESISE)
@@ -308,6 +337,29 @@ def main():
         dom_ms = sum(evd.elapsed_ms(evd.ev[2 * i], evd.ev[2 * i + 1]) for i in range(K)) / K
         evd.close()
 
+    # the same step captured once into a HIP graph and replayed (the paper
+    # times round trips under graph replay); the chain records no memsets
+    graph_ms = None
+    if not args.no_graph:
+        cur = torch.cuda.current_stream()
+        side = torch.cuda.Stream()
+        side.wait_stream(cur)
+        with torch.cuda.stream(side):
+            step()
+        cur.wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        for _ in range(W):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(K):
+            g.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - t0) * 1e3 / K
+        del g
+
     if args.copy_calib_mb:
         src = torch.empty(args.copy_calib_mb * 1024 * 1024 // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -321,19 +373,19 @@ def main():
     x64 = x_np.astype(np.float64)
     snr = 10 * np.log10(np.sum(x64 ** 2, axis=1) / np.sum((x64 - xr_np) ** 2, axis=1))
 
-    N, C, b = w.n_samples, plan.n_coeffs, w.batch
+    N, C = plan.n_samples, plan.n_coeffs
     b_alg = (24.0 * N + 16.0 * C) * b              # method's algorithmic bytes per round trip
     value = b * N / (ms * 1e-3)
     out = {
         "metric": METRIC, "value": value, "unit": "samples/s", "n_gpus": 1, "steps": K, "warmup": W,
         "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
-        "config": {"workload": f"{w.name}: {b} x {N} samples @ {w.fs:g} Hz, {w.fmin:g} Hz..fs/2, "
-                               f"{w.bins_per_octave} bins/oct, analysis+synthesis round trip",
+        "config": {"workload": describe(w, b, N) + ", analysis+synthesis round trip",
                    "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": C},
         "pct_hbm_peak": 100.0 * b_alg / (ms * 1e-3) / HBM_PEAK,
         "alg_bytes_per_step": b_alg,
         "snr_db_min": float(snr.min()),
+        "graph_replay_ms_per_step": graph_ms,
         "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_synthesise) / b,
     }
     if dom is not None:
@@ -341,10 +393,47 @@ def main():
         out["roofline"] = {"bound": "hbm", "kernel": names[dom], "kernel_ms": round(dom_ms, 5),
                            "achieved": round(achieved, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                            "frac": achieved / (HBM_PEAK / 1e9),
-                           "traffic": traffic_from_profiles(w.name, names[dom])}
+                           "traffic": traffic_from_profiles(w.name, names[dom]) if b == w.batch else None}
         out["stages"] = stages
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x_np)
+    print(json.dumps(out), flush=True)
+
+
+def bench_step(args, w, plan, x):
+    """Eager differentiable round trip: xr = S T x, L = sum (xr - t)^2, and
+    L.backward() through the explicit adjoints (T^dagger S^dagger)."""
+    import torch
+    import workloads
+    from paper_2609_29119_amd import autograd as ag
+    b, N = x.shape
+    t = torch.from_numpy(workloads.white(w.cot_seed, b, N)).cuda()
+    cqt = ag.CQT(plan)
+
+    def step():
+        xg = x.detach().requires_grad_()
+        loss = ((cqt.inverse(cqt(xg)) - t) ** 2).sum()
+        loss.backward()
+        return xg.grad
+
+    K, W = args.steps, args.warmup
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        g = step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / K
+    # the gradient is T^dagger S^dagger 2 (S T x - t) ~ 2 T^dagger S^dagger (x - t)
+    out = {"metric": "CQT differentiable round-trip step (eager: T, S, squared error, backward through "
+                     "the adjoints) audio samples/s",
+           "value": b * N / (ms * 1e-3), "unit": "samples/s", "n_gpus": 1, "steps": K, "warmup": W,
+           "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "f32", "data": "synthetic",
+           "config": {"workload": describe(w, b, N) + ", differentiable round-trip step",
+                      "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": plan.n_coeffs},
+           "grad_finite": bool(torch.isfinite(g).all().item())}
     print(json.dumps(out), flush=True)
 
 

@@ -17,6 +17,9 @@ does not name their content, so these stand in for it):
           sliced mode uses slices of 2**17 with 50 % overlap
   stress  128 x 88,200 @ 22.05 kHz, 8 sinusoids + Bernoulli(1e-3) +-1
           impulses + N(0, 0.05) noise; 55 Hz..fs/2, 36 bins/oct
+  table1  128 x 65,536 @ 44.1 kHz, N(0,1) noise; the multi-resolution band
+          list of the paper's Table 1 (the shape of its own measurements,
+          whose signal content it does not state)
 
 N(mu, v) is read with v the variance. Every signal of a batch gets its own
 child generator from ``SeedSequence(seed).spawn(batch)``; values are drawn in
@@ -41,6 +44,7 @@ class Workload:
     seed: int
     cot_seed: int
     slice_len: int = 0          # 0: no sliced mode for this workload
+    layout: str = "cq"          # "cq": constant-Q from (fs, fmin, fmax, B); "table1": Table 1 band list
 
     @property
     def plan_args(self):
@@ -54,6 +58,7 @@ WORKLOADS = {
     "long": Workload("long", 48000.0, 20.0, 24000.0, 96, 2880000, 1, 4, 1004,
                      slice_len=131072),
     "stress": Workload("stress", 22050.0, 55.0, 11025.0, 36, 88200, 128, 5, 1005),
+    "table1": Workload("table1", 44100.0, 0.0, 0.0, 0, 65536, 128, 6, 1006, layout="table1"),
 }
 
 
@@ -85,7 +90,7 @@ def _pink(rng, n, fs):
 def signal_row(w: Workload, rng, n=None):
     """One fp64 signal of the workload's recipe from one child generator."""
     n = w.n_samples if n is None else n
-    if w.name in ("tiny", "long"):
+    if w.name in ("tiny", "long", "table1"):
         return rng.standard_normal(n)
     if w.name == "single":
         return _sinusoids(rng, n, w.fs, 30.0, 18000.0) + rng.normal(0.0, np.sqrt(0.01), n)
