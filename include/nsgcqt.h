@@ -205,6 +205,20 @@ int nsgcqt_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t n_samples
 int nsgcqt_layout_table1(nsgcqt_band_spec* out, int capacity, int* n_bands, double* fs,
                          int64_t* n_samples);
 
+/* An auditory layout (another painless nonstationary Gabor frame, built like
+ * the constant-Q one on the ERB-rate scale of Glasberg and Moore:
+ * ERB(f) = 24.7 (4.37 f/1000 + 1) Hz, E(f) = 21.4 log10(1 + 4.37 f/1000)).
+ * Positive centres f_j with E(f_j) = E(fmin) + j / bands_per_erb, kept while
+ * f_j <= fmax and f_j < fs/2; Hann windows of half-amplitude width
+ * ERB(f_j) / bands_per_erb (the centre spacing); DC and Nyquist sidebands
+ * complementing the outer Hann halves; lengths = support widths; bands with
+ * empty support left out. Fills *n_bands and, with out non-NULL, the bands
+ * (capacity >= *n_bands, else EINVAL), for nsgcqt_plan_create_bands.
+ * EINVAL: n_bands NULL, N odd or < 4, fs <= 0, fmin <= 0, fmin >= fs/2,
+ *         fmax < fmin, bands_per_erb not in (0, 1000]. */
+int nsgcqt_layout_erb(double fs, int64_t n_samples, double fmin, double fmax, double bands_per_erb,
+                      nsgcqt_band_spec* out, int capacity, int* n_bands);
+
 /* Free the plan and its device tables. Any work using it must have
  * completed. NULL is accepted. */
 int nsgcqt_plan_destroy(nsgcqt_plan plan);

@@ -17,14 +17,15 @@ Everything follows the plain definitions of Sec. 2 of the paper:
 
 Parity status of each function is stated in its module header.
 """
-from .layout import Band, Layout, build_layout, build_band_layout, table1_specs
+from .layout import (Band, Layout, build_layout, build_band_layout, table1_specs, erb_specs, erb_hz,
+                     erb_rate)
 from .nsgt import (analyse, analyse_bands, synthesise, adjoint_analysis, adjoint_synthesis,
                    band_idft, band_dft, split_bands)
 from .sliced import slice_window, slice_count, sliced_analyse, sliced_synthesise
 from .metrics import snr_db, rel_l2
 
 __all__ = [
-    "Band", "Layout", "build_layout", "build_band_layout", "table1_specs",
+    "Band", "Layout", "build_layout", "build_band_layout", "table1_specs", "erb_specs", "erb_hz", "erb_rate",
     "analyse", "analyse_bands", "synthesise", "adjoint_analysis", "adjoint_synthesis",
     "band_idft", "band_dft", "split_bands",
     "slice_window", "slice_count", "sliced_analyse", "sliced_synthesise",

@@ -30,7 +30,9 @@ given centres and widths with lengths M >= the support width: the slots past
 the support hold zero, which is the band spectrum zero-padded to M (Sec. 2
 only asks that E_lambda place the support injectively into M slots).
 ``table1_specs`` is the multi-resolution layout of Table 1 (Sec. 4) under the
-reading stated in its docstring.
+reading stated in its docstring, and ``erb_specs`` an auditory layout on the
+ERB-rate scale (another painless frame of the kind Sec. 6 says the
+construction extends to).
 
 Parity: pinned by tests (closed-form windows, sum h g = 1, coverage bounds,
 band counts, agreement with an independent integer layout).
@@ -247,3 +249,36 @@ def table1_specs():
     specs += [(POSITIVE, xi, beta, length[o], xi * fs / N) for xi, beta, o in zip(xis, betas, octave)]
     specs.append((NYQUIST, xis[-1], betas[-1], 2048, fs / 2.0))
     return fs, N, specs
+
+
+def erb_hz(f):
+    """Equivalent rectangular bandwidth (Glasberg and Moore, 1990) in Hz."""
+    return 24.7 * (4.37 * f / 1000.0 + 1.0)
+
+
+def erb_rate(f):
+    """ERB-rate (number of ERBs below f) of the same model."""
+    return 21.4 * math.log10(1.0 + 4.37 * f / 1000.0)
+
+
+def erb_specs(fs, N, fmin, fmax, per_erb):
+    """Auditory layout: centres one 1/per_erb apart on the ERB-rate scale from
+    fmin (while <= fmax and below fs/2), Hann windows whose half-amplitude
+    width is the centre spacing ERB(f)/per_erb, sidebands complementing the
+    outer Hann halves, lengths equal to the support widths; bands without a
+    bin inside their support are left out."""
+    half = N // 2
+    e0 = erb_rate(fmin)
+    pos = []
+    j = 0
+    while True:
+        f = (10.0 ** ((e0 + j / per_erb) / 21.4) - 1.0) * 1000.0 / 4.37
+        if not (f <= fmax * (1.0 + 1e-12) and f < fs / 2.0):
+            break
+        xi = f * N / fs
+        beta = erb_hz(f) / per_erb * N / fs
+        if min(half, math.ceil(xi + beta) - 1) >= max(0, math.floor(xi - beta) + 1):
+            pos.append((POSITIVE, xi, beta, 0, f))
+        j += 1
+    return [(DC, pos[0][1], pos[0][2], 0, 0.0)] + pos + [(NYQUIST, pos[-1][1], pos[-1][2], 0, fs / 2.0)]
+

@@ -442,6 +442,22 @@ int create_bands(nsgcqt_plan* out, double fs, int64_t n, int batch, int n_bands,
     });
 }
 
+// Band count to *n and, with out non-NULL, the bands (capacity permitting).
+int copy_specs(const std::vector<BandSpec>& specs, nsgcqt_band_spec* out, int capacity, int* n) {
+    *n = static_cast<int>(specs.size());
+    if (!out) return NSGCQT_OK;
+    if (capacity < static_cast<int>(specs.size()))
+        return set_err(NSGCQT_EINVAL, "capacity below the " + std::to_string(specs.size()) + " bands of the layout");
+    for (size_t i = 0; i < specs.size(); ++i) {
+        out[i].kind = specs[i].kind;
+        out[i].xi = specs[i].xi;
+        out[i].beta = specs[i].beta;
+        out[i].length = specs[i].M;
+        out[i].centre_hz = specs[i].f;
+    }
+    return NSGCQT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -479,20 +495,23 @@ int nsgcqt_layout_table1(nsgcqt_band_spec* out, int capacity, int* n_bands, doub
     if (!n_bands) return set_err(NSGCQT_EINVAL, "n_bands is NULL");
     std::vector<BandSpec> specs;
     table1_specs(specs);
-    *n_bands = static_cast<int>(specs.size());
     if (fs) *fs = kTable1Fs;
     if (n_samples) *n_samples = kTable1N;
-    if (!out) return NSGCQT_OK;
-    if (capacity < static_cast<int>(specs.size()))
-        return set_err(NSGCQT_EINVAL, "capacity below the " + std::to_string(specs.size()) + " bands of the layout");
-    for (size_t i = 0; i < specs.size(); ++i) {
-        out[i].kind = specs[i].kind;
-        out[i].xi = specs[i].xi;
-        out[i].beta = specs[i].beta;
-        out[i].length = specs[i].M;
-        out[i].centre_hz = specs[i].f;
+    return copy_specs(specs, out, capacity, n_bands);
+}
+
+int nsgcqt_layout_erb(double fs, int64_t n_samples, double fmin, double fmax, double bands_per_erb,
+                      nsgcqt_band_spec* out, int capacity, int* n_bands) {
+    if (!n_bands) return set_err(NSGCQT_EINVAL, "n_bands is NULL");
+    std::vector<BandSpec> specs;
+    std::string err;
+    try {
+        if (int r = erb_specs(fs, n_samples, fmin, fmax, bands_per_erb, specs, err)) return set_err(r, err);
+    } catch (const std::bad_alloc&) {
+        return set_err(NSGCQT_ENOMEM, "host allocation failed");
     }
-    return NSGCQT_OK;
+    if (specs.size() > static_cast<size_t>(INT32_MAX / 2)) return set_err(NSGCQT_EUNSUPPORTED, "too many bands");
+    return copy_specs(specs, out, capacity, n_bands);
 }
 
 int nsgcqt_plan_destroy(nsgcqt_plan p) {

@@ -475,6 +475,43 @@ void table1_specs(std::vector<BandSpec>& out) {
     out.push_back(BandSpec{2, pos.back().xi, pos.back().beta, 2048, fs / 2.0});
 }
 
+int erb_specs(double fs, int64_t N, double fmin, double fmax, double v, std::vector<BandSpec>& out,
+              std::string& err) {
+    out.clear();
+    if (!(N >= 4) || (N % 2) != 0) return fail(err, NSGCQT_EINVAL, "n_samples must be even and >= 4");
+    if (!(fs > 0.0)) return fail(err, NSGCQT_EINVAL, "fs must be > 0");
+    if (!(fmin > 0.0) || !(fmin < fs / 2.0)) return fail(err, NSGCQT_EINVAL, "fmin must satisfy 0 < fmin < fs/2");
+    if (!(fmax >= fmin)) return fail(err, NSGCQT_EINVAL, "fmax must be >= fmin");
+    if (!(v > 0.0) || !(v <= 1e3)) return fail(err, NSGCQT_EINVAL, "bands per ERB must be in (0, 1000]");
+    // Glasberg and Moore: ERB(f) = 24.7 (4.37 f / 1000 + 1) Hz and the
+    // ERB-rate E(f) = 21.4 log10(1 + 4.37 f / 1000)
+    auto erb = [](double f) { return 24.7 * (4.37 * f / 1000.0 + 1.0); };
+    auto rate = [](double f) { return 21.4 * std::log10(1.0 + 4.37 * f / 1000.0); };
+    auto inv_rate = [](double e) { return (std::pow(10.0, e / 21.4) - 1.0) * 1000.0 / 4.37; };
+    const double Nd = static_cast<double>(N), e0 = rate(fmin);
+    const int64_t half = N / 2;
+    std::vector<BandSpec> pos;
+    for (int64_t j = 0;; ++j) {
+        const double f = inv_rate(e0 + static_cast<double>(j) / v);
+        if (!(f <= fmax * (1.0 + 1e-12) && f < fs / 2.0)) break;
+        if (j > 1000000) return fail(err, NSGCQT_EUNSUPPORTED, "more than a million bands");
+        BandSpec s{};
+        s.kind = 1;
+        s.xi = f * Nd / fs;
+        s.beta = erb(f) / v * Nd / fs;
+        s.M = 0;
+        s.f = f;
+        const int64_t lo = std::max<int64_t>(0, static_cast<int64_t>(std::floor(s.xi - s.beta)) + 1);
+        const int64_t hi = std::min<int64_t>(half, static_cast<int64_t>(std::ceil(s.xi + s.beta)) - 1);
+        if (hi >= lo) pos.push_back(s);
+    }
+    if (pos.empty()) return fail(err, NSGCQT_EINVAL, "no band between fmin and fmax");
+    out.push_back(BandSpec{0, pos.front().xi, pos.front().beta, 0, 0.0});
+    out.insert(out.end(), pos.begin(), pos.end());
+    out.push_back(BandSpec{2, pos.back().xi, pos.back().beta, 0, fs / 2.0});
+    return NSGCQT_OK;
+}
+
 namespace {
 
 int finish_plan(HostPlan& p, std::string& err) {

@@ -119,6 +119,14 @@ constexpr int64_t kTable1N = 65536;
 constexpr double kTable1Fs = 44100.0;
 void table1_specs(std::vector<BandSpec>& out);
 
+// An auditory (ERB-rate) layout for N samples at fs: positive centres
+// equally spaced by 1/v on the ERB-rate scale from fmin while <= fmax and
+// below fs/2, Hann windows whose half-amplitude width is the centre spacing
+// ERB(f)/v, sidebands as in the constant-Q layout, lengths = support widths.
+// Bands with empty support are left out. Returns 0 or a negative status.
+int erb_specs(double fs, int64_t N, double fmin, double fmax, double v, std::vector<BandSpec>& out,
+              std::string& err);
+
 // Radix factorisation used by the Stockham stages: primes above 16 (at most
 // max_prime) become stages of their own, the remaining factors are packed
 // greedily into radices of at most 16. False when n has a larger prime factor

@@ -28,7 +28,7 @@ EXPORTS = [
     "nsgcqt_adjoint", "nsgcqt_sliced_count", "nsgcqt_sliced_analyse",
     "nsgcqt_sliced_synthesise", "nsgcqt_set_stage_events", "nsgcqt_stage_info",
     "nsgcqt_last_error", "nsgcqt_plan_create_bands", "nsgcqt_plan_create_bands_host",
-    "nsgcqt_layout_table1",
+    "nsgcqt_layout_table1", "nsgcqt_layout_erb",
 ]
 
 
@@ -97,6 +97,7 @@ def lib():
         "nsgcqt_plan_create_bands_host": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
         "nsgcqt_layout_table1": [ctypes.POINTER(BandSpec), I, ctypes.POINTER(ctypes.c_int),
                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
+        "nsgcqt_layout_erb": [D, I64, D, D, D, ctypes.POINTER(BandSpec), I, ctypes.POINTER(ctypes.c_int)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -334,3 +335,15 @@ def table1_layout():
     arr = (BandSpec * n.value)()
     _check(L.nsgcqt_layout_table1(arr, n.value, ctypes.byref(n), None, None))
     return fs.value, N.value, [b.as_tuple() for b in arr]
+
+
+def erb_layout(fs, n_samples, fmin, fmax, bands_per_erb=1.0):
+    """The auditory (ERB-rate) layout of nsgcqt_layout_erb as band tuples."""
+    L = lib()
+    n = ctypes.c_int()
+    args = (float(fs), int(n_samples), float(fmin), float(fmax), float(bands_per_erb))
+    _check(L.nsgcqt_layout_erb(*args, None, 0, ctypes.byref(n)))
+    arr = (BandSpec * n.value)()
+    _check(L.nsgcqt_layout_erb(*args, arr, n.value, ctypes.byref(n)))
+    return [b.as_tuple() for b in arr]
+

@@ -350,3 +350,20 @@ def test_band_list_rejections(lib):
     assert lib.nsgcqt_layout_table1((nb.BandSpec * 10)(), 10, ctypes.byref(n), None, None) == nb.EINVAL
     assert n.value == 154
 
+
+def test_erb_preset_identical_to_oracle(lib):
+    args = (16000.0, 32000, 50.0, 8000.0, 2.0)
+    specs = nb.erb_layout(*args)
+    ospecs = oracle.erb_specs(*args)
+    assert len(specs) == len(ospecs)
+    for a, b in zip(specs, ospecs):
+        assert a[0] == b[0] and a[3] == b[3]
+        np.testing.assert_allclose(a[1:3] + a[4:], b[1:3] + b[4:], rtol=1e-13)
+    p = nb.Plan.from_bands(16000.0, 32000, specs, batch=1, device=False)
+    lay = oracle.build_band_layout(16000.0, 32000, ospecs)
+    assert [(b.k_lo, b.k_hi, b.k_centre, b.length) for b in p.bands()] == \
+           [(b.k_lo, b.k_hi, b.k_c, b.M) for b in lay.bands]
+    n = ctypes.c_int()
+    assert lib.nsgcqt_layout_erb(16000.0, 32000, 50.0, 8000.0, 0.0, None, 0, ctypes.byref(n)) == nb.EINVAL
+    assert lib.nsgcqt_layout_erb(16000.0, 32000, 9000.0, 9500.0, 1.0, None, 0, ctypes.byref(n)) == nb.EINVAL
+

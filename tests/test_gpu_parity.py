@@ -294,6 +294,18 @@ def test_band_list_against_oracle(case):
     _check_all_ops(p, lay, x, y, xs_, mode=mode)
 
 
+def test_erb_layout_against_oracle():
+    # an auditory (ERB-rate) frame through the band-list plan
+    fs, N, b = 16000.0, 32000, 2
+    specs = nb.erb_layout(fs, N, 50.0, 8000.0, 2.0)
+    lay = oracle.build_band_layout(fs, N, specs)
+    p = nb.Plan.from_bands(fs, N, specs, batch=b)
+    x = workloads.white(16001, b, N)
+    y = workloads.coeff_cotangent(16002, b, p.n_coeffs)
+    xs = workloads.signal_cotangent(16003, b, N)
+    _check_all_ops(p, lay, x, y, xs)
+
+
 def test_autograd_gradients_against_oracle():
     # gradients through T and S and the differentiable round trip of the
     # paper's second experiment (squared error against a target, backprop

@@ -413,6 +413,45 @@ def test_band_list_rejections():
         oracle.build_band_layout(40.0, N, good[:2])
 
 
+def test_erb_scale_values():
+    # Glasberg and Moore (1990): ERB(1 kHz) = 24.7 * 5.37 = 132.639 Hz and
+    # 21.4 log10(5.37) = 15.621 ERBs below 1 kHz; ERB(0) = 24.7 Hz
+    assert oracle.erb_hz(1000.0) == pytest.approx(132.639, abs=1e-9)
+    assert oracle.erb_hz(0.0) == pytest.approx(24.7)
+    assert oracle.erb_rate(1000.0) == pytest.approx(15.6214, abs=1e-4)
+    # dE/df = 1.0032 / ERB(f) (the scale counts ERBs)
+    f = 3000.0
+    d = (oracle.erb_rate(f + 1e-3) - oracle.erb_rate(f - 1e-3)) / 2e-3
+    assert d * oracle.erb_hz(f) == pytest.approx(21.4 * 4.37 / 1000 / math.log(10) * 24.7, rel=1e-6)
+
+
+def test_erb_layout_spacing_and_frame():
+    fs, N, v = 16000.0, 4000, 2.0
+    specs = oracle.erb_specs(fs, N, 50.0, 8000.0, v)
+    lay = oracle.build_band_layout(fs, N, specs)
+    pos = [b for b in lay.bands if b.kind == POSITIVE]
+    rates = np.array([oracle.erb_rate(b.centre_hz) for b in pos])
+    # every kept centre sits on the 1/v grid of the ERB-rate scale
+    steps = (rates - oracle.erb_rate(50.0)) * v
+    np.testing.assert_allclose(steps, np.round(steps), atol=1e-9)
+    # half-amplitude width = ERB / v; the next centre lies a fixed ratio of it
+    # away: f' - f = (f + 1000/4.37)(10^(1/(21.4 v)) - 1) and
+    # ERB(f) = 24.7 (4.37/1000)(f + 1000/4.37)
+    for b in pos:
+        assert b.beta == pytest.approx(oracle.erb_hz(b.centre_hz) / v * N / fs, rel=1e-12)
+    sp = np.diff([b.xi for b in pos])
+    w = np.array([b.beta for b in pos[:-1]])
+    ratio = (10 ** (1 / (21.4 * v)) - 1) * v / (24.7 * 4.37 / 1000)
+    np.testing.assert_allclose(sp / w, ratio, rtol=1e-9)
+    assert abs(ratio - 1) < 0.03
+    # a painless frame: S T = I, adjoint identity (library-FFT band mode)
+    x = np.random.default_rng(21).standard_normal(N)
+    c = oracle.analyse(lay, x)
+    assert oracle.snr_db(x, oracle.synthesise(lay, c)) > 250
+    y = np.random.default_rng(22).standard_normal(lay.n_coeffs) * (1 + 0j)
+    assert np.sum(np.real(np.conj(c) * y)) == pytest.approx(np.sum(x * oracle.adjoint_analysis(lay, y)), rel=1e-11)
+
+
 # ---------------------------------------------------------------- sliced mode
 
 def test_slice_window_partition_of_unity():
