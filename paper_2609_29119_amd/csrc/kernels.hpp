@@ -434,6 +434,10 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
+    // the descriptor in LDS: the stage loop then issues no global loads
+    __shared__ FftDesc fdl;
+    for (int i = threadIdx.x; i < static_cast<int>(sizeof(FftDesc) / 4); i += NT)
+        reinterpret_cast<int*>(&fdl)[i] = reinterpret_cast<const int*>(fd)[i];
     float2* buf = lds;
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
@@ -483,11 +487,11 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
+    lds_fft<NT, EPT>(buf, S, lg, &fdl, T.tw);
     if (blu) {
         blu_middle<NT>(buf, n, lg, S, sg, T.kern + bd.kern);
         __syncthreads();
-        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
+        lds_fft<NT, EPT>(buf, S, lg, &fdl, T.tw);
     }
     if (!live) return;
     float2* cb = coef + (long long)it.s0 * C + bd.off;
@@ -522,6 +526,9 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
     if (g <= 0) return;
     const BandDev bd = T.bands[it.band];
     const FftDesc* fd = T.ffts + bd.fft;
+    __shared__ FftDesc fdl;
+    for (int i = threadIdx.x; i < static_cast<int>(sizeof(FftDesc) / 4); i += NT)
+        reinterpret_cast<int*>(&fdl)[i] = reinterpret_cast<const int*>(fd)[i];
     float2* buf = lds;
     const int M = bd.M, n = fd->n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
@@ -547,11 +554,11 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
     __syncthreads();
-    lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
+    lds_fft<NT, EPT>(buf, S, lg, &fdl, T.tw);
     if (blu) {
         blu_middle<NT>(buf, n, lg, S, sg, T.kern + bd.kern);
         __syncthreads();
-        lds_fft<NT, EPT>(buf, S, lg, fd, T.tw);
+        lds_fft<NT, EPT>(buf, S, lg, &fdl, T.tw);
     }
     if (!live) return;
     const float* w = wt + bd.off;
