@@ -193,6 +193,18 @@ int nsgcqt_plan_create_bands(nsgcqt_plan* out, double fs, int64_t n_samples, int
 int nsgcqt_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t n_samples, int batch,
                                   int n_bands, const nsgcqt_band_spec* bands);
 
+/* Sliced (streaming) plan of an explicit band list for slices of slice_len
+ * samples (a multiple of 8), with the slicing of nsgcqt_sliced_plan_create
+ * (Sec. 4 streams the Table 1 layout this way). The bands are in bins of
+ * the length-slice_len DFT. Errors as for nsgcqt_plan_create_bands, and
+ * EINVAL for a slice length that is not a multiple of 8. */
+int nsgcqt_sliced_plan_create_bands(nsgcqt_plan* out, double fs, int64_t slice_len, int slices_per_chunk,
+                                    int n_bands, const nsgcqt_band_spec* bands);
+
+/* Host-only variant of nsgcqt_sliced_plan_create_bands. */
+int nsgcqt_sliced_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t slice_len,
+                                         int slices_per_chunk, int n_bands, const nsgcqt_band_spec* bands);
+
 /* The multi-resolution layout of Table 1 (Sec. 4): N = 65,536 at 44.1 kHz;
  * octaves 1-3 at 8, 4-7 at 16 and 8-9 at 32 bands per octave above a lowest
  * centre of 64 bins (43.07 Hz), centres rounded to bins and the highest one

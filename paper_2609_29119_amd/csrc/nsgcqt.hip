@@ -430,7 +430,7 @@ auto cq_builder(double fs, double fmin, double fmax, int bpo, int64_t n, int bat
 }
 
 int create_bands(nsgcqt_plan* out, double fs, int64_t n, int batch, int n_bands, const nsgcqt_band_spec* bands,
-                 bool device) {
+                 bool sliced, bool device) {
     if (out) *out = nullptr;
     if (n_bands < 1) return set_err(NSGCQT_EINVAL, "n_bands must be >= 1");
     if (!bands) return set_err(NSGCQT_EINVAL, "bands is NULL");
@@ -438,7 +438,7 @@ int create_bands(nsgcqt_plan* out, double fs, int64_t n, int batch, int n_bands,
     for (int i = 0; i < n_bands; ++i)
         specs[i] = BandSpec{bands[i].kind, bands[i].xi, bands[i].beta, bands[i].length, bands[i].centre_hz};
     return create(out, device, [&](HostPlan& h, std::string& err) {
-        return build_host_plan_bands(h, fs, n, batch, specs, err);
+        return build_host_plan_bands(h, fs, n, batch, specs, sliced, err);
     });
 }
 
@@ -483,12 +483,22 @@ int nsgcqt_sliced_plan_create_host(nsgcqt_plan* out, double fs, double fmin, dou
 
 int nsgcqt_plan_create_bands(nsgcqt_plan* out, double fs, int64_t n_samples, int batch, int n_bands,
                              const nsgcqt_band_spec* bands) {
-    return create_bands(out, fs, n_samples, batch, n_bands, bands, true);
+    return create_bands(out, fs, n_samples, batch, n_bands, bands, false, true);
 }
 
 int nsgcqt_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t n_samples, int batch, int n_bands,
                                   const nsgcqt_band_spec* bands) {
-    return create_bands(out, fs, n_samples, batch, n_bands, bands, false);
+    return create_bands(out, fs, n_samples, batch, n_bands, bands, false, false);
+}
+
+int nsgcqt_sliced_plan_create_bands(nsgcqt_plan* out, double fs, int64_t slice_len, int slices_per_chunk,
+                                    int n_bands, const nsgcqt_band_spec* bands) {
+    return create_bands(out, fs, slice_len, slices_per_chunk, n_bands, bands, true, true);
+}
+
+int nsgcqt_sliced_plan_create_bands_host(nsgcqt_plan* out, double fs, int64_t slice_len, int slices_per_chunk,
+                                         int n_bands, const nsgcqt_band_spec* bands) {
+    return create_bands(out, fs, slice_len, slices_per_chunk, n_bands, bands, true, false);
 }
 
 int nsgcqt_layout_table1(nsgcqt_band_spec* out, int capacity, int* n_bands, double* fs, int64_t* n_samples) {

@@ -371,8 +371,8 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int B,
 }
 
 int build_host_plan_bands(HostPlan& p, double fs, int64_t N, int batch, const std::vector<BandSpec>& specs,
-                          std::string& err) {
-    if (int r = begin_plan(p, fs, N, batch, false, err)) return r;
+                          bool sliced, std::string& err) {
+    if (int r = begin_plan(p, fs, N, batch, sliced, err)) return r;
     p.fmin = 0.0; p.fmax = 0.0; p.bpo = 0;
     if (specs.empty()) return fail(err, NSGCQT_EINVAL, "the band list is empty");
     if (specs.size() >= (size_t(1) << 24)) return fail(err, NSGCQT_EUNSUPPORTED, "too many bands");

@@ -111,8 +111,9 @@ int build_host_plan(HostPlan& p, double fs, double fmin, double fmax, int bpo,
                     int64_t N, int batch, bool sliced, std::string& err);
 
 // Plan of an explicit band list (see BandSpec); same return convention.
+// sliced: N is the slice length and batch the slices per chunk.
 int build_host_plan_bands(HostPlan& p, double fs, int64_t N, int batch, const std::vector<BandSpec>& specs,
-                          std::string& err);
+                          bool sliced, std::string& err);
 
 // The multi-resolution layout of the paper's Table 1 (N = 65,536 at 44.1 kHz).
 constexpr int64_t kTable1N = 65536;

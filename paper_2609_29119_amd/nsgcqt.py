@@ -28,7 +28,8 @@ EXPORTS = [
     "nsgcqt_adjoint", "nsgcqt_sliced_count", "nsgcqt_sliced_analyse",
     "nsgcqt_sliced_synthesise", "nsgcqt_set_stage_events", "nsgcqt_stage_info",
     "nsgcqt_last_error", "nsgcqt_plan_create_bands", "nsgcqt_plan_create_bands_host",
-    "nsgcqt_layout_table1", "nsgcqt_layout_erb",
+    "nsgcqt_layout_table1", "nsgcqt_layout_erb", "nsgcqt_sliced_plan_create_bands",
+    "nsgcqt_sliced_plan_create_bands_host",
 ]
 
 
@@ -95,6 +96,8 @@ def lib():
         "nsgcqt_last_error": [],
         "nsgcqt_plan_create_bands": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
         "nsgcqt_plan_create_bands_host": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
+        "nsgcqt_sliced_plan_create_bands": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
+        "nsgcqt_sliced_plan_create_bands_host": [pp, D, I64, I, I, ctypes.POINTER(BandSpec)],
         "nsgcqt_layout_table1": [ctypes.POINTER(BandSpec), I, ctypes.POINTER(ctypes.c_int),
                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
         "nsgcqt_layout_erb": [D, I64, D, D, D, ctypes.POINTER(BandSpec), I, ctypes.POINTER(ctypes.c_int)],
@@ -139,7 +142,10 @@ class Plan:
         h = ctypes.c_void_p()
         if _bands is not None:
             arr = (BandSpec * len(_bands))(*[BandSpec(*b) for b in _bands])
-            fn = L.nsgcqt_plan_create_bands if device else L.nsgcqt_plan_create_bands_host
+            if _sliced:
+                fn = L.nsgcqt_sliced_plan_create_bands if device else L.nsgcqt_sliced_plan_create_bands_host
+            else:
+                fn = L.nsgcqt_plan_create_bands if device else L.nsgcqt_plan_create_bands_host
             _check(fn(ctypes.byref(h), float(fs), int(n_samples), int(batch), len(_bands), arr))
         else:
             if _sliced:
@@ -163,6 +169,12 @@ class Plan:
         """Plan of an explicit band list: tuples (kind, xi, beta, length[, centre_hz])
         as nsgcqt_band_spec, in coefficient order."""
         return cls(fs, 0.0, 0.0, 0, n_samples, batch, device, _bands=[tuple(b) for b in bands])
+
+    @classmethod
+    def sliced_from_bands(cls, fs, slice_len, bands, slices_per_chunk=16, device=True):
+        """Sliced (streaming) plan of an explicit band list for slices of slice_len."""
+        return cls(fs, 0.0, 0.0, 0, slice_len, slices_per_chunk, device, _sliced=True,
+                   _bands=[tuple(b) for b in bands])
 
     def close(self):
         if getattr(self, "_h", None):

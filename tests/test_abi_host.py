@@ -367,3 +367,15 @@ def test_erb_preset_identical_to_oracle(lib):
     assert lib.nsgcqt_layout_erb(16000.0, 32000, 50.0, 8000.0, 0.0, None, 0, ctypes.byref(n)) == nb.EINVAL
     assert lib.nsgcqt_layout_erb(16000.0, 32000, 9000.0, 9500.0, 1.0, None, 0, ctypes.byref(n)) == nb.EINVAL
 
+
+def test_sliced_band_list_plan(lib):
+    fs, N, specs = nb.table1_layout()
+    p = nb.Plan.sliced_from_bands(fs, N, specs, 8, device=False)
+    assert p.info.sliced == 1 and p.n_coeffs == 132992
+    assert p.slice_count(2646000) == oracle.slice_count(2646000, N)
+    arr = (nb.BandSpec * len(specs))(*[nb.BandSpec(*b) for b in specs])
+    h = ctypes.c_void_p()
+    # a slice length that is not a multiple of 8
+    assert lib.nsgcqt_sliced_plan_create_bands_host(ctypes.byref(h), fs, N + 2, 8, len(specs), arr) == nb.EINVAL
+    assert not h.value
+

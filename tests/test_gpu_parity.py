@@ -167,6 +167,23 @@ def test_sliced_mode_against_oracle():
     np.testing.assert_array_less(oracle.rel_l2(xr, oracle.sliced_synthesise(lay, cref, n)), 1e-5)
 
 
+def test_sliced_table1_layout_against_oracle():
+    # Sec. 4 streams its Table 1 layout in slices of 65,536 samples
+    fs, Ns, specs = nb.table1_layout()
+    lay = oracle.build_band_layout(fs, Ns, specs)
+    p = nb.Plan.sliced_from_bands(fs, Ns, specs, 4)
+    n = 210001                       # 8 slices in chunks of 4, odd length
+    x = workloads.white(44100, 1, n)[0]
+    c = p.sliced_analyse(to_gpu(x))
+    cg = to_np(c)
+    cref = oracle.sliced_analyse(lay, x, mode="fft")
+    assert cg.shape == cref.shape
+    assert np.all(np.linalg.norm(cref, axis=1) > 0)
+    assert oracle.rel_l2(cg, cref).max() <= REL_TOL
+    xr = to_np(p.sliced_synthesise(c, n))
+    assert oracle.snr_db(x, xr) >= SNR_MIN
+
+
 def test_sliced_long_full_length():
     # the 60 s workload: 45 slices in chunks of 16; oracle on sampled slices,
     # reconstruction over the whole signal
