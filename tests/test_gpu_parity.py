@@ -42,6 +42,11 @@ def to_np(t):
 # tiles, ragged tails, odd packed lengths, prime-radix (matrix-core) stages in
 # the bands and in the packed FFT (L = 2 * 67, 2 * 257), and Bluestein bands
 SMALL = [
+    # degenerate sizes: N = 4 (L = 2, bands of length 1), L = 3, L = 15
+    ("N4_min", 4.0, 0.5, 2.0, 1, 4, 2),
+    ("N6_L3", 6.0, 0.7, 3.0, 1, 6, 2),
+    ("N8", 8.0, 1.0, 4.0, 1, 8, 1),
+    ("N30_L15", 30.0, 1.0, 15.0, 2, 30, 3),
     ("N500_L250", 250.0, 4.0, 125.0, 4, 500, 2),
     ("N268_L2x67", 268.0, 4.0, 134.0, 4, 268, 2),
     ("N1028_L2x257", 1028.0, 8.0, 514.0, 6, 1028, 3),
