@@ -11,7 +11,11 @@ stress workload). Prints one JSON line.
 
 --mode step times the differentiable round trip of the paper's second
 experiment instead (eager: T, S, squared error against a target, and the
-backward pass through the explicit adjoints).
+backward pass through the explicit adjoints). --mode fwdbwd times analysis
+T followed by its adjoint T^dagger on a random cotangent (the training
+front end). --workload long times the full-length round trip of the 60 s
+signal and the sliced round trip (slices of 2^17, 50 % overlap), with the
+peak workspace of each.
 """
 from __future__ import annotations
 
@@ -225,7 +229,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="stress")
     ap.add_argument("--batch", type=int, default=0, help="signals per step (default: the workload's)")
-    ap.add_argument("--mode", choices=("roundtrip", "step"), default="roundtrip")
+    ap.add_argument("--mode", choices=("roundtrip", "step", "fwdbwd"), default="roundtrip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
     ap.add_argument("--no-stage-events", action="store_true",
@@ -251,7 +255,7 @@ def main():
 
     w = workloads.WORKLOADS[args.workload]
     if w.slice_len:
-        raise SystemExit("bench runs full-length workloads; use the sliced tests for the long one")
+        return bench_long(args, w)
     b = args.batch or w.batch
     torch.cuda.init()
     plan = make_plan(w, b)
@@ -259,6 +263,8 @@ def main():
     x = torch.from_numpy(x_np).cuda()
     if args.mode == "step":
         return bench_step(args, w, plan, x)
+    if args.mode == "fwdbwd":
+        return bench_fwdbwd(args, w, plan, x)
     c = torch.empty((b, plan.n_coeffs), dtype=torch.complex64, device="cuda")
     xr = torch.empty_like(x)
     ws_a = plan.workspace(nc.OP_ANALYSE)
@@ -434,6 +440,116 @@ def bench_step(args, w, plan, x):
            "config": {"workload": describe(w, b, N) + ", differentiable round-trip step",
                       "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": plan.n_coeffs},
            "grad_finite": bool(torch.isfinite(g).all().item())}
+    print(json.dumps(out), flush=True)
+
+
+
+def _timed(fn, K, W):
+    """Mean wall time per call of fn over K calls after W warm-up calls, with
+    the device synchronised on both sides (ms)."""
+    import torch
+    for _ in range(W):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / K
+
+
+def bench_fwdbwd(args, w, plan, x):
+    """Analysis T x, then T^dagger y for a fixed random coefficient cotangent y."""
+    import torch
+    import workloads
+    import paper_2609_29119_amd as nc
+    b, N = x.shape
+    C = plan.n_coeffs
+    y = torch.from_numpy(workloads.coeff_cotangent(w.cot_seed, b, C)).cuda()
+    c = torch.empty((b, C), dtype=torch.complex64, device="cuda")
+    g = torch.empty_like(x)
+    ws_a, ws_t = plan.workspace(nc.OP_ANALYSE), plan.workspace(nc.OP_ADJ_ANALYSIS)
+
+    def step():
+        plan.analyse(x, out=c, ws=ws_a)
+        plan.adjoint(nc.OP_ADJ_ANALYSIS, y, out=g, ws=ws_t)
+
+    ms = _timed(step, args.steps, args.warmup)
+    b_alg = (24.0 * N + 16.0 * C) * b      # T: 12N + 8C, T^dagger: 12N + 8C
+    out = {"metric": "CQT analysis forward + adjoint backward audio samples/s and % HBM peak",
+           "value": b * N / (ms * 1e-3), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": describe(w, b, N) + ", analysis T then adjoint T^dagger",
+                      "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": C},
+           "pct_hbm_peak": 100.0 * b_alg / (ms * 1e-3) / HBM_PEAK, "alg_bytes_per_step": b_alg,
+           "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_adjoint_analysis) / b}
+    print(json.dumps(out), flush=True)
+
+
+def bench_long(args, w):
+    """The 60 s signal: full-length round trip and sliced round trip, each
+    with its plan's workspace and the device-memory high-water mark of the
+    call beyond its inputs and outputs."""
+    import torch
+    import workloads
+    import paper_2609_29119_amd as nc
+    torch.cuda.init()
+    x_np = workloads.signals(w)
+    x = torch.from_numpy(x_np).cuda()
+    N = w.n_samples
+    res = {}
+    # full length: one plan over all N samples
+    plan = nc.Plan(*w.plan_args, batch=1)
+    c = torch.empty((1, plan.n_coeffs), dtype=torch.complex64, device="cuda")
+    xr = torch.empty_like(x)
+    ws_a, ws_s = plan.workspace(nc.OP_ANALYSE), plan.workspace(nc.OP_SYNTHESISE)
+
+    def full():
+        plan.analyse(x, out=c, ws=ws_a)
+        plan.synthesise(c, out=xr, ws=ws_s)
+
+    ms = _timed(full, args.steps, args.warmup)
+    e = (x_np[0].astype(np.float64) - xr.cpu().numpy()[0])
+    snr = 10 * np.log10(np.sum(x_np.astype(np.float64) ** 2) / np.sum(e ** 2))
+    res["full"] = {"ms_per_step": ms, "samples_per_s": N / (ms * 1e-3), "snr_db": float(snr),
+                   "n_bands": plan.n_bands, "n_coeffs": plan.n_coeffs,
+                   "workspace_bytes": max(plan.info.ws_analyse, plan.info.ws_synthesise),
+                   "table_bytes": plan.info.table_bytes,
+                   "pct_hbm_peak": 100.0 * (24.0 * N + 16.0 * plan.n_coeffs) / (ms * 1e-3) / HBM_PEAK}
+    del plan, c, xr, ws_a, ws_s
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    # sliced: slices of slice_len, 50 % overlap, 16 slices per chunk
+    sp = nc.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16)
+    x1 = x[0].contiguous()
+    J = sp.slice_count(N)
+    cs = torch.empty((J, sp.n_coeffs), dtype=torch.complex64, device="cuda")
+    xs = torch.empty_like(x1)
+    wa, wsn = sp.workspace(nc.OP_ANALYSE), sp.workspace(nc.OP_SYNTHESISE)
+
+    def sliced():
+        sp.sliced_analyse(x1, out=cs, ws=wa)
+        sp.sliced_synthesise(cs, N, out=xs, ws=wsn)
+
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    ms = _timed(sliced, args.steps, args.warmup)
+    peak = torch.cuda.max_memory_allocated() - base
+    e = x_np[0].astype(np.float64) - xs.cpu().numpy()
+    snr = 10 * np.log10(np.sum(x_np.astype(np.float64) ** 2) / np.sum(e ** 2))
+    res["sliced"] = {"ms_per_step": ms, "samples_per_s": N / (ms * 1e-3), "snr_db": float(snr),
+                     "slices": J, "slice_len": w.slice_len, "coeffs_per_slice": sp.n_coeffs,
+                     "workspace_bytes": max(sp.info.ws_analyse, sp.info.ws_synthesise),
+                     "table_bytes": sp.info.table_bytes, "alloc_peak_during_calls_bytes": int(peak)}
+    out = {"metric": "CQT analysis+synthesis round-trip audio samples/s (full-length and sliced); peak workspace",
+           "value": res["full"]["samples_per_s"], "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": res["full"]["ms_per_step"], "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": f"{w.name}: 1 x {N} samples @ {w.fs:g} Hz, {w.fmin:g} Hz..fs/2, "
+                                  f"{w.bins_per_octave} bins/oct, full-length and sliced round trips"},
+           **res}
     print(json.dumps(out), flush=True)
 
 

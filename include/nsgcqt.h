@@ -45,9 +45,14 @@
  *   - A plan owns its device tables (allocated on the device current at
  *     creation, freed by nsgcqt_plan_destroy). Plans are immutable: calls on
  *     different streams with distinct workspaces may run concurrently.
- *   - Compute calls only enqueue work on `stream` (a hipStream_t, NULL for
- *     the default stream); they never synchronise the host and may be
- *     captured into a HIP graph. They are not in-place.
+ *   - Compute calls only enqueue work (a hipStream_t, NULL for the default
+ *     stream); they never synchronise the host and may be captured into a
+ *     HIP graph. They are not in-place. When every band launch of a plan is
+ *     small (few signals), independent launches of one call also run on the
+ *     plan's own side streams, which wait for the work already on `stream`
+ *     and which `stream` waits for before the call's later work: the call
+ *     stays ordered on `stream` as one unit. Calls on one plan from several
+ *     streams share those side streams and may partly serialise.
  *
  * Errors
  *   Every function returns an nsgcqt_status. No C++ exception crosses the

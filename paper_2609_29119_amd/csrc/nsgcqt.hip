@@ -51,6 +51,16 @@ struct nsgcqt_plan_s {
     std::vector<hipEvent_t> events;
     int ev_next = 0;
     std::map<const void*, int> resident;   // persistent kernels: workgroups resident at once
+    // independent launches of one call (band tiers, the huge-band chain) run
+    // concurrently on the caller's stream and these side streams (default
+    // priority), forked from and joined back into the caller's stream
+    static constexpr int kSide = 3;
+    hipStream_t side[kSide] = {};
+    hipEvent_t fork_ev = nullptr;
+    hipEvent_t join_ev[kSide] = {};
+    // only when every band launch is small: launches that fill the GPU on
+    // their own lose more to contention than they gain from overlap
+    bool fan = false;
 };
 
 namespace {
@@ -118,18 +128,71 @@ int upload(nsgcqt_plan_s* p) {
     p->wSa = static_cast<const float*>(at(iWSa));
     p->rA = static_cast<const float4*>(at(iRA));
     p->rSa = static_cast<const float4*>(at(iRSa));
+    for (int i = 0; i < nsgcqt_plan_s::kSide; ++i) {
+        HIP_TRY(hipStreamCreateWithFlags(&p->side[i], hipStreamNonBlocking));
+        HIP_TRY(hipEventCreateWithFlags(&p->join_ev[i], hipEventDisableTiming));
+    }
+    HIP_TRY(hipEventCreateWithFlags(&p->fork_ev, hipEventDisableTiming));
+    int most = 0;
+    for (const auto& bk : h.buckets) most = std::max(most, bk.nitems);
+    p->fan = most < 2048;
     p->device = true;
     return NSGCQT_OK;
 }
 
-// Releases the plan's device tables.
+// Releases the plan's device tables, side streams and events.
 int release(nsgcqt_plan_s* p) {
-    if (!p->dmem) return NSGCQT_OK;
-    const hipError_t e = hipFree(p->dmem);
+    hipError_t e = hipSuccess;
+    auto keep = [&](hipError_t r) { if (e == hipSuccess) e = r; };
+    for (int i = 0; i < nsgcqt_plan_s::kSide; ++i) {
+        if (p->side[i]) keep(hipStreamDestroy(p->side[i]));
+        if (p->join_ev[i]) keep(hipEventDestroy(p->join_ev[i]));
+        p->side[i] = nullptr;
+        p->join_ev[i] = nullptr;
+    }
+    if (p->fork_ev) keep(hipEventDestroy(p->fork_ev));
+    p->fork_ev = nullptr;
+    if (p->dmem) keep(hipFree(p->dmem));
     p->dmem = nullptr;
-    if (e != hipSuccess) return set_err(NSGCQT_EDEVICE, std::string("hipFree: ") + hipGetErrorString(e));
+    if (e != hipSuccess) return set_err(NSGCQT_EDEVICE, std::string("release: ") + hipGetErrorString(e));
     return NSGCQT_OK;
 }
+
+// Spreads independent launches over the caller's stream s and the plan's
+// side streams: unit u runs on s when u % 4 == 0, else on side stream
+// u % 4 - 1, which first waits for the work already on s; join() makes s
+// wait for every side stream used.
+struct Fanout {
+    nsgcqt_plan_s* p;
+    hipStream_t s;
+    bool forked = false;
+    bool used[nsgcqt_plan_s::kSide] = {};
+    int stream(int u, hipStream_t* out) {
+        const int k = p->fan ? u % (nsgcqt_plan_s::kSide + 1) : 0;
+        if (k == 0) {
+            *out = s;
+            return NSGCQT_OK;
+        }
+        if (!forked) {
+            HIP_TRY(hipEventRecord(p->fork_ev, s));
+            forked = true;
+        }
+        if (!used[k - 1]) {
+            HIP_TRY(hipStreamWaitEvent(p->side[k - 1], p->fork_ev, 0));
+            used[k - 1] = true;
+        }
+        *out = p->side[k - 1];
+        return NSGCQT_OK;
+    }
+    int join() {
+        for (int i = 0; i < nsgcqt_plan_s::kSide; ++i)
+            if (used[i]) {
+                HIP_TRY(hipEventRecord(p->join_ev[i], p->side[i]));
+                HIP_TRY(hipStreamWaitEvent(s, p->join_ev[i], 0));
+            }
+        return NSGCQT_OK;
+    }
+};
 
 // ---------------------------------------------------------------- launches
 template <typename K>
@@ -274,10 +337,14 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
 
 // The band tiers, one launch each.
 // Analysis reads the router factors rt, synthesis the weights wt.
+// Bucket i runs as fanout unit i.
 int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float4* rt, const float* wt,
-              int batch, hipStream_t s) {
+              int batch, Fanout& fan) {
     const HostPlan& h = p->h;
-    for (const auto& bk : h.buckets) {
+    for (size_t bi = 0; bi < h.buckets.size(); ++bi) {
+        const Bucket& bk = h.buckets[bi];
+        hipStream_t s;
+        if (int r = fan.stream(static_cast<int>(bi), &s)) return r;
         const int lds = bk.lds_elems * static_cast<int>(sizeof(float2));
         const dim3 grid(bk.nitems), block(bk.nt);
         auto go = [&](auto ka, auto ks) -> int {
@@ -351,12 +418,18 @@ int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float4
     float2* Z = reinterpret_cast<float2*>(ws + align256(8 * h.L * batch));
     if (int r = run_fwd_a(p, x, Y, batch, sl, static_cast<long long>(h.N), s)) return r;
     if (int r = run_pass_b<false>(p, Y, Z, batch, static_cast<long long>(h.L), s)) return r;
-    if (int r = run_bands(p, true, Z, coeffs, rt, nullptr, batch, s)) return r;
+    Fanout fan{p, s};
+    if (int r = run_bands(p, true, Z, coeffs, rt, nullptr, batch, fan)) return r;
     BigArgs a = big_args(p, ws, h.off_h_an, h.spc ? h.spc : batch, true);
     a.Z = Z;
     a.cout = coeffs;
     a.rt = rt;
-    return run_big(p, a, batch, s);
+    if (!h.bigs.empty()) {
+        hipStream_t sb;
+        if (int r = fan.stream(static_cast<int>(h.buckets.size()), &sb)) return r;
+        if (int r = run_big(p, a, batch, sb)) return r;
+    }
+    return fan.join();
 }
 
 // Synthesis chain (S, or T^dagger with its weights); output is [batch][N] f32.
@@ -365,12 +438,18 @@ int chain_synthesise(nsgcqt_plan_s* p, const float2* coeffs, float* xo, const fl
     const HostPlan& h = p->h;
     float2* W = reinterpret_cast<float2*>(ws);
     float2* Y = reinterpret_cast<float2*>(ws + align256(8 * h.C * batch));
-    if (int r = run_bands(p, false, coeffs, W, nullptr, wt, batch, s)) return r;
+    Fanout fan{p, s};
+    if (int r = run_bands(p, false, coeffs, W, nullptr, wt, batch, fan)) return r;
     BigArgs a = big_args(p, ws, h.off_h_syn, h.spc ? h.spc : batch, false);
     a.cin = coeffs;
     a.W = W;
     a.wt = wt;
-    if (int r = run_big(p, a, batch, s)) return r;
+    if (!h.bigs.empty()) {
+        hipStream_t sb;
+        if (int r = fan.stream(static_cast<int>(h.buckets.size()), &sb)) return r;
+        if (int r = run_big(p, a, batch, sb)) return r;
+    }
+    if (int r = fan.join()) return r;
     if (int r = run_inv_a(p, W, Y, batch, s)) return r;
     return run_pass_b<true>(p, Y, reinterpret_cast<float2*>(xo), batch, static_cast<long long>(h.L), s);
 }
