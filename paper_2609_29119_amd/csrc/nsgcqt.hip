@@ -366,7 +366,8 @@ int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, co
         if (bk.nt == 64) r = go(k_band_analysis<64, 8>, k_band_synthesis<64, 8>);
         else if (bk.nt == 256 && bk.ept == 8) r = go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
         else if (bk.nt == 256) r = go(k_band_analysis<256, 16>, k_band_synthesis<256, 16>);
-        else r = go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
+        else if (bk.nt == 512) r = go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
+        else r = go(k_band_analysis<1024, 16>, k_band_synthesis<1024, 16>);
         if (r) return r;
     }
     return NSGCQT_OK;

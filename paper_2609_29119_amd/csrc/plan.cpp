@@ -180,7 +180,7 @@ int fail(std::string& err, int code, const std::string& msg) {
 
 // Band kernel tiers by transform length: threads and elements per thread.
 struct Tier { int max_work, nt, ept; };
-constexpr Tier kTiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}};
+constexpr Tier kTiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}, {16384, 1024, 16}};
 constexpr int kNumTiers = static_cast<int>(sizeof(kTiers) / sizeof(kTiers[0]));
 
 int tier_of(int64_t n) {
