@@ -58,8 +58,8 @@ struct nsgcqt_plan_s {
     hipStream_t side[kSide] = {};
     hipEvent_t fork_ev = nullptr;
     hipEvent_t join_ev[kSide] = {};
-    // only when every band launch is small: launches that fill the GPU on
-    // their own lose more to contention than they gain from overlap
+    // only for plans whose band launches are all small and whose band phase
+    // is long (see upload)
     bool fan = false;
 };
 
@@ -128,14 +128,23 @@ int upload(nsgcqt_plan_s* p) {
     p->wSa = static_cast<const float*>(at(iWSa));
     p->rA = static_cast<const float4*>(at(iRA));
     p->rSa = static_cast<const float4*>(at(iRSa));
+    // the fork and join events order work within this device only
+    const unsigned evf = hipEventDisableTiming | hipEventDisableSystemFence;
     for (int i = 0; i < nsgcqt_plan_s::kSide; ++i) {
         HIP_TRY(hipStreamCreateWithFlags(&p->side[i], hipStreamNonBlocking));
-        HIP_TRY(hipEventCreateWithFlags(&p->join_ev[i], hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&p->join_ev[i], evf));
     }
-    HIP_TRY(hipEventCreateWithFlags(&p->fork_ev, hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&p->fork_ev, evf));
+    // overlap pays when no band launch fills the GPU by itself and the band
+    // phase is long against the fork and join (~25 us each way): at least
+    // 6M element slots of band work
     int most = 0;
-    for (const auto& bk : h.buckets) most = std::max(most, bk.nitems);
-    p->fan = most < 2048;
+    double work = 4.0 * static_cast<double>(h.Hn) * static_cast<double>(h.batch);
+    for (const auto& bk : h.buckets) {
+        most = std::max(most, bk.nitems);
+        work += static_cast<double>(bk.nitems) * bk.nt * bk.ept;
+    }
+    p->fan = most < 2048 && work >= 6e6;
     p->device = true;
     return NSGCQT_OK;
 }

@@ -395,6 +395,41 @@ def test_graph_capture_replays_match_eager():
         assert np.array_equal(to_np(xr).view(np.uint32), xe.view(np.uint32)), i
 
 
+def test_graph_capture_with_side_streams():
+    # the training plan (16 signals, no band launch filling the GPU, a long
+    # band phase) forks its band launches onto the plan's side streams; the
+    # captured round trip, with the side streams joined into the capture,
+    # replays bitwise equal to the eager one
+    w = workloads.WORKLOADS["train"]
+    b, N = w.batch, w.n_samples
+    p = nb.Plan(*w.plan_args, batch=b)
+    x = to_gpu(workloads.white(52, b, N))
+    ce = to_np(p.analyse(x))
+    xe = to_np(p.synthesise(to_gpu(ce)))
+    c = torch.empty((b, p.n_coeffs), dtype=torch.complex64, device="cuda")
+    xr = torch.empty_like(x)
+    ws_a, ws_s = p.workspace(nb.OP_ANALYSE), p.workspace(nb.OP_SYNTHESISE)
+    cur = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(cur)
+    with torch.cuda.stream(side):
+        p.analyse(x, out=c, ws=ws_a)
+        p.synthesise(c, out=xr, ws=ws_s)
+    cur.wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        p.analyse(x, out=c, ws=ws_a)
+        p.synthesise(c, out=xr, ws=ws_s)
+    for i in range(3):
+        c.zero_()
+        xr.zero_()
+        p.synthesise(p.analyse(to_gpu(workloads.white(70 + i, b, N))))
+        torch.cuda.synchronize()
+        g.replay()
+        assert np.array_equal(to_np(c).view(np.uint32), ce.view(np.uint32)), i
+        assert np.array_equal(to_np(xr).view(np.uint32), xe.view(np.uint32)), i
+
+
 def test_workspace_too_small_raises():
     w = workloads.WORKLOADS["tiny"]
     p = nb.Plan(*w.plan_args, batch=1)
