@@ -43,8 +43,10 @@
  *     caller. The workspace size comes from nsgcqt_plan_info(); the library
  *     never allocates during a compute call.
  *   - A plan owns its device tables (allocated on the device current at
- *     creation, freed by nsgcqt_plan_destroy). Plans are immutable: calls on
- *     different streams with distinct workspaces may run concurrently.
+ *     creation, freed by nsgcqt_plan_destroy). A plan's layout and tables
+ *     are immutable. Calls on one plan from several host threads take turns
+ *     while they enqueue (a per-plan lock); their work on different streams
+ *     with distinct workspaces may then run concurrently on the device.
  *   - Compute calls only enqueue work (a hipStream_t, NULL for the default
  *     stream); they never synchronise the host and may be captured into a
  *     HIP graph. They are not in-place. When every band launch of a plan is

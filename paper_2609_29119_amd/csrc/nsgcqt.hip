@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -61,6 +62,9 @@ struct nsgcqt_plan_s {
     // only for plans whose band launches are all small and whose band phase
     // is long (see upload)
     bool fan = false;
+    // the enqueue state above (events, the resident-block cache, the fork and
+    // join events) is used by one call at a time
+    std::mutex mu;
 };
 
 namespace {
@@ -679,6 +683,7 @@ int nsgcqt_plan_weights(nsgcqt_plan p, int which, float* dst, size_t bytes) {
 
 int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_t ws_bytes, void* stream) {
     if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, false)) return r;
+    std::lock_guard<std::mutex> lock(p->mu);
     p->ev_next = 0;
     return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->rA, p->h.batch, SliceIn{0, 0, 0, 0},
                          static_cast<char*>(ws), static_cast<hipStream_t>(stream));
@@ -686,6 +691,7 @@ int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_
 
 int nsgcqt_synthesise(nsgcqt_plan p, const float* coeffs, float* xo, void* ws, size_t ws_bytes, void* stream) {
     if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, false)) return r;
+    std::lock_guard<std::mutex> lock(p->mu);
     p->ev_next = 0;
     return chain_synthesise(p, reinterpret_cast<const float2*>(coeffs), xo, p->wS, p->h.batch,
                             static_cast<char*>(ws), static_cast<hipStream_t>(stream));
@@ -696,6 +702,7 @@ int nsgcqt_adjoint(nsgcqt_plan p, int op, const float* in, float* out, void* ws,
         return set_err(NSGCQT_EINVAL, "op must be NSGCQT_OP_ADJ_ANALYSIS or NSGCQT_OP_ADJ_SYNTHESIS");
     const bool ta = op == NSGCQT_OP_ADJ_ANALYSIS;
     if (int r = check_call(p, in, out, ws, ws_bytes, p ? (ta ? p->h.ws_syn : p->h.ws_an) : 0, false)) return r;
+    std::lock_guard<std::mutex> lock(p->mu);
     p->ev_next = 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (ta)
@@ -716,6 +723,7 @@ int nsgcqt_sliced_analyse(nsgcqt_plan p, const float* x, int64_t n, float* coeff
                           void* stream) {
     if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, true)) return r;
     if (n < 1) return set_err(NSGCQT_EINVAL, "signal length must be >= 1");
+    std::lock_guard<std::mutex> lock(p->mu);
     const HostPlan& h = p->h;
     const int64_t J = nsgcqt_sliced_count(p, n);
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -733,6 +741,7 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, floa
                              size_t ws_bytes, void* stream) {
     if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, true)) return r;
     if (n < 1) return set_err(NSGCQT_EINVAL, "signal length must be >= 1");
+    std::lock_guard<std::mutex> lock(p->mu);
     const HostPlan& h = p->h;
     const int64_t J = nsgcqt_sliced_count(p, n);
     const int64_t H = h.N / 2;
@@ -762,6 +771,7 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, floa
 
 int nsgcqt_set_stage_events(nsgcqt_plan p, void* const* events, int n_events) {
     if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
+    std::lock_guard<std::mutex> lock(p->mu);
     p->events.clear();
     p->ev_next = 0;
     if (events && n_events > 0)

@@ -430,6 +430,41 @@ def test_graph_capture_with_side_streams():
         assert np.array_equal(to_np(xr).view(np.uint32), xe.view(np.uint32)), i
 
 
+def test_concurrent_calls_from_threads():
+    # two host threads drive one plan (the training plan, whose calls fork
+    # onto the plan's side streams) on their own streams and workspaces; every
+    # result equals the single-threaded one bitwise
+    import threading
+    w = workloads.WORKLOADS["train"]
+    b, N = w.batch, w.n_samples
+    p = nb.Plan(*w.plan_args, batch=b)
+    xs = [to_gpu(workloads.white(80 + i, b, N)) for i in range(2)]
+    refs = [to_np(p.analyse(x)) for x in xs]
+    need = p.info.ws_analyse
+    outs = [torch.empty((b, p.n_coeffs), dtype=torch.complex64, device="cuda") for _ in range(2)]
+    wss = [torch.empty(need, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    errors = []
+
+    def run(i):
+        try:
+            for _ in range(5):
+                p.analyse(xs[i], out=outs[i], ws=wss[i], stream=streams[i])
+        except Exception as e:          # reported by the main thread
+            errors.append(e)
+
+    torch.cuda.synchronize()
+    ts = [threading.Thread(target=run, args=(i,)) for i in range(2)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for i in range(2):
+        assert np.array_equal(to_np(outs[i]).view(np.uint32), refs[i].view(np.uint32)), i
+
+
 def test_workspace_too_small_raises():
     w = workloads.WORKLOADS["tiny"]
     p = nb.Plan(*w.plan_args, batch=1)
