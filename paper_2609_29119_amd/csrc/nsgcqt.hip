@@ -62,6 +62,7 @@ struct nsgcqt_plan_s {
     // only for plans whose band launches are all small and whose band phase
     // is long (see upload)
     bool fan = false;
+    std::vector<int> lane;   // stream of each launch unit (buckets, then the huge-band chain): 0 = caller's
     // the enqueue state above (events, the resident-block cache, the fork and
     // join events) is used by one call at a time
     std::mutex mu;
@@ -149,6 +150,24 @@ int upload(nsgcqt_plan_s* p) {
         work += static_cast<double>(bk.nitems) * bk.nt * bk.ept;
     }
     p->fan = most < 2048 && work >= 6e6;
+    // longest first onto the least loaded of the four streams
+    {
+        std::vector<double> cost;
+        for (const auto& bk : h.buckets) cost.push_back(static_cast<double>(bk.nitems) * bk.nt * bk.ept);
+        cost.push_back(4.0 * static_cast<double>(h.Hn) * static_cast<double>(h.batch));
+        std::vector<int> order(cost.size());
+        for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
+        std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cost[a] > cost[b]; });
+        double load[nsgcqt_plan_s::kSide + 1] = {};
+        p->lane.assign(cost.size(), 0);
+        for (int u : order) {
+            int best = 0;
+            for (int k = 1; k <= nsgcqt_plan_s::kSide; ++k)
+                if (load[k] < load[best]) best = k;
+            p->lane[u] = best;
+            load[best] += cost[u];
+        }
+    }
     p->device = true;
     return NSGCQT_OK;
 }
@@ -172,8 +191,8 @@ int release(nsgcqt_plan_s* p) {
 }
 
 // Spreads independent launches over the caller's stream s and the plan's
-// side streams: unit u runs on s when u % 4 == 0, else on side stream
-// u % 4 - 1, which first waits for the work already on s; join() makes s
+// side streams: unit u runs on s when its lane is 0, else on side stream
+// lane - 1, which first waits for the work already on s; join() makes s
 // wait for every side stream used.
 struct Fanout {
     nsgcqt_plan_s* p;
@@ -181,7 +200,7 @@ struct Fanout {
     bool forked = false;
     bool used[nsgcqt_plan_s::kSide] = {};
     int stream(int u, hipStream_t* out) {
-        const int k = p->fan ? u % (nsgcqt_plan_s::kSide + 1) : 0;
+        const int k = p->fan ? p->lane[u] : 0;
         if (k == 0) {
             *out = s;
             return NSGCQT_OK;
