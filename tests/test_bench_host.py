@@ -1,0 +1,47 @@
+"""CPU checks of the benchmark's host logic (no GPU needed)."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    msg = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "one GPU" in msg["error"]
+
+
+@pytest.mark.parametrize("name,stage", [
+    ("void nsg::k_fwd_a<512, 8, false>(float const*, ...)", "fft_fwd_a"),
+    ("void nsg::k_pass_b<512, 8, false>(...)", "fft_fwd_b"),
+    ("void nsg::k_pass_b<512, 8, true>(...)", "fft_inv_b"),
+    ("void nsg::k_inv_a<512, 8>(...)", "fft_inv_a_overlap_add"),
+    ("void nsg::k_band_analysis<256, 8>(...)", "band_analysis_256x8"),
+    ("void nsg::k_band_synthesis<1024, 16>(...)", "band_synthesis_1024x16"),
+    ("__amd_rocclr_copyBuffer", None),
+])
+def test_profiler_kernel_names_map_to_stages(name, stage):
+    assert bench.stage_of_kernel(name) == stage
+
+
+def test_traffic_is_null_for_other_sources(tmp_path, monkeypatch):
+    # counters taken on other kernel sources are not reported
+    current = bench.kernel_source_hash()
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / "traffic_x.json").write_text(json.dumps(
+        {"source_hash": "0" * 16, "kernels": {"k": {"hbm_bytes_per_launch": 1.0}}}))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: current)
+    assert bench.traffic_from_profiles("x", "k") is None
+    (prof / "traffic_x.json").write_text(json.dumps(
+        {"source_hash": current, "kernels": {"k": {"hbm_bytes_per_launch": 5.0}}}))
+    assert bench.traffic_from_profiles("x", "k") == 5.0
