@@ -22,9 +22,9 @@ namespace nsg {
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
 // caps each kernel at 256 VGPRs per lane.
 #define NSG_OCC __attribute__((amdgpu_waves_per_eu(2)))
-// The 256 x 8 band kernels carry most of the band work and gain from six
-// waves per SIMD (at most 80 VGPRs, no spills); the others do not.
-#define NSG_OCC_BAND __attribute__((amdgpu_waves_per_eu((NT == 256 && EPT == 8) ? 6 : 2)))
+// The 256 x 8 and 64 x 8 band kernels gain from six waves per SIMD (at most
+// 80 VGPRs, no spills); the larger tiers do not.
+#define NSG_OCC_BAND __attribute__((amdgpu_waves_per_eu(((NT == 256 || NT == 64) && EPT == 8) ? 6 : 2)))
 
 struct Tables {
     const BandDev* bands;
