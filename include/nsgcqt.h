@@ -152,7 +152,9 @@ typedef struct {
  *         fmax < fmin, bins_per_octave < 1, batch < 1, or a bin that no band
  *         covers (a_k = 0, Sec. 2).
  * EUNSUPPORTED: N >= 2^29 (rows are addressed with 32-bit byte offsets);
- *         L = N/2 has a prime factor above 257, the largest Stockham radix;
+ *         L = N/2 has a prime factor above 257, the largest Stockham radix,
+ *         or its two-pass split does not fit a workgroup's LDS (L above
+ *         about 10^7; L = 2^23 fits);
  *         or a band transform beyond one workgroup has no split n = n1 n2
  *         with n1 <= n2 <= 4096 into such radices. Bands never need their
  *         length's prime factors to be small: Bluestein's algorithm covers

@@ -33,7 +33,7 @@ struct Tables {
     const float2* omega;     // exp(-2 pi i k / N), k = 0..L
     const int32_t* owner;    // first band covering bin k | count << 24, k = 0..L
     const int32_t* bandbase; // off - k_lo per band
-    const int4* gather;      // per bin k = 0..L: covering bands of k and of L - k (head, steps) x 2
+    const int4* gather;      // per bin k = 0..L: covering bands of k and of L - k (one or two int4)
     const float2* chirp;     // Bluestein exp(-i pi m^2 / M)
     const float2* kern;      // Bluestein DFT_P(b) / P
     const float2* tw4_hi;
@@ -225,6 +225,15 @@ __device__ __forceinline__ float2 gather_bin(const float2* __restrict__ Ws, int 
     return make_float2(a.x + mb * b.x + mc * c.x, a.y + mb * b.y + mc * c.y);
 }
 
+// The same sum from a wide half-record: `head` as above, i1 and i2 the
+// second and third bands' absolute W indices (the first's where absent).
+__device__ __forceinline__ float2 gather_bin_abs(const float2* __restrict__ Ws, int head, int i1, int i2) {
+    const int i0 = head & ((1 << 29) - 1), cnt = static_cast<int>(static_cast<unsigned>(head) >> 29);
+    const float2 a = at32(Ws, i0), b = at32(Ws, i1), c = at32(Ws, i2);
+    const float mb = cnt > 1 ? 1.f : 0.f, mc = cnt > 2 ? 1.f : 0.f;
+    return make_float2(a.x + mb * b.x + mc * c.x, a.y + mb * b.y + mc * c.y);
+}
+
 // ------------------------------- inverse packed FFT, pass A, with overlap-add
 // X_q for the packed bins of a tile is summed from the bands that cover the
 // bin (no atomics: every packed bin is produced by exactly one thread), made
@@ -245,7 +254,8 @@ __device__ __forceinline__ float2 retangle_conj(float2 om, float2 xq, float2 xm)
     return make_float2(0.5f * z.x, -0.5f * z.y);          // conj(Z)
 }
 
-template <int NT, int EPT>
+// WIDE: the plan's bin records are the 32-byte form (absolute indices).
+template <int NT, int EPT, bool WIDE>
 __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__ W, float2* __restrict__ Y,
                                                       Pass p, Tables T, int batch, long long C) {
     extern __shared__ float2 lds[];
@@ -267,20 +277,30 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     // into the tile
     constexpr int U = 4;
     for (int base = threadIdx.x; base < tot; base += U * NT) {
-        int4 g[U];
+        int4 g[U], g2[U];
         float2 oq[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int e = min(base + u * NT, tot - 1);
             const int q = __mul24(e >> lgH, p.L2) + c0 + min(e & (H - 1), ncols - 1);
-            g[u] = at32(T.gather, q);      // bins q and L - q
+            if constexpr (WIDE) {
+                g[u] = at32(T.gather, 2 * q);      // bins q and L - q
+                g2[u] = at32(T.gather, 2 * q + 1);
+            } else {
+                g[u] = at32(T.gather, q);          // bins q and L - q
+            }
             oq[u] = at32(T.omega, q);
         }
         float2 xq[U], xm[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            xq[u] = gather_bin(Ws, g[u].x, g[u].y);
-            xm[u] = gather_bin(Ws, g[u].z, g[u].w);
+            if constexpr (WIDE) {
+                xq[u] = gather_bin_abs(Ws, g[u].x, g[u].y, g[u].z);
+                xm[u] = gather_bin_abs(Ws, g[u].w, g2[u].x, g2[u].y);
+            } else {
+                xq[u] = gather_bin(Ws, g[u].x, g[u].y);
+                xm[u] = gather_bin(Ws, g[u].z, g[u].w);
+            }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {

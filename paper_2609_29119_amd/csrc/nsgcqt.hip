@@ -342,7 +342,11 @@ int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream
         ev_end(p, s);
         return NSGCQT_OK;
     };
-    DISPATCH_NT(p->h.fs4.nt_a, k_inv_a)
+    if (p->h.gather_wide) {
+        DISPATCH_NT(p->h.fs4.nt_a, k_inv_a, , true)
+    } else {
+        DISPATCH_NT(p->h.fs4.nt_a, k_inv_a, , false)
+    }
     return NSGCQT_OK;
 }
 

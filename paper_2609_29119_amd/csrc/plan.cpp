@@ -602,32 +602,42 @@ int finish_plan(HostPlan& p, std::string& err) {
     p.bandbase.resize(p.bands.size());
     for (size_t l = 0; l < p.bands.size(); ++l)
         p.bandbase[l] = static_cast<int32_t>(p.bands[l].off - p.bands[l].k_lo);
-    // per bin k, one 16-byte record for the bin and its mirror L - k, so the
-    // overlap-add reads both with one table load: for each side the W index
+    // per bin k, one record for the bin and its mirror L - k, so the
+    // overlap-add reads both with one table load. For each side: the W index
     // (within one signal's row) of the first covering band with the count in
-    // its top 3 bits, then the steps to the second and third bands' W indices
-    // as two int16 (0 where there is no such band)
+    // its top 3 bits, then the second and third bands' W indices. Compact
+    // (16 bytes): those two as int16 steps from the previous index (0 where
+    // there is no such band). Wide (32 bytes, when a step does not fit 16
+    // bits): absolute indices, the first band's where there is no such band;
+    // layout head_k, i1_k, i2_k, head_m | i1_m, i2_m, 0, 0.
     if (p.max_overlap > 3) return fail(err, NSGCQT_EUNSUPPORTED, "more than three bands cover one bin");
     if (p.C >= (int64_t(1) << 29)) return fail(err, NSGCQT_EUNSUPPORTED, "2^29 coefficients or more");
-    p.gather.assign(4 * (half + 1), 0);
     {
-        std::vector<int32_t> head(half + 1), steps(half + 1);
+        std::vector<int32_t> head(half + 1), i1(half + 1), i2(half + 1), steps(half + 1);
+        bool wide = false;
         for (int64_t k = 0; k <= half; ++k) {
             const int first = p.owner[k] & 0xFFFFFF, cnt = p.owner[k] >> 24;
             int64_t idx[3] = {0, 0, 0};
             for (int j = 0; j < cnt; ++j) idx[j] = p.bandbase[first + j] + k;
             const int64_t d1 = cnt > 1 ? idx[1] - idx[0] : 0, d2 = cnt > 2 ? idx[2] - idx[1] : 0;
-            if (d1 < -32768 || d1 > 32767 || d2 < -32768 || d2 > 32767)
-                return fail(err, NSGCQT_EUNSUPPORTED, "overlapping bands too far apart in the coefficient row");
+            if (d1 < -32768 || d1 > 32767 || d2 < -32768 || d2 > 32767) wide = true;
             head[k] = static_cast<int32_t>(idx[0] | (static_cast<int64_t>(cnt) << 29));
+            i1[k] = static_cast<int32_t>(cnt > 1 ? idx[1] : idx[0]);
+            i2[k] = static_cast<int32_t>(cnt > 2 ? idx[2] : idx[0]);
             steps[k] = static_cast<int32_t>((d1 & 0xFFFF) | (static_cast<uint32_t>(d2 & 0xFFFF) << 16));
         }
+        p.gather_wide = wide;
+        p.gather.assign((wide ? 8 : 4) * (half + 1), 0);
         for (int64_t k = 0; k <= half; ++k) {
             const int64_t m = L - k;   // mirror bin (0 <-> L)
-            p.gather[4 * k + 0] = head[k];
-            p.gather[4 * k + 1] = steps[k];
-            p.gather[4 * k + 2] = head[m];
-            p.gather[4 * k + 3] = steps[m];
+            if (wide) {
+                int32_t* r = p.gather.data() + 8 * k;
+                r[0] = head[k]; r[1] = i1[k]; r[2] = i2[k]; r[3] = head[m];
+                r[4] = i1[m]; r[5] = i2[m];
+            } else {
+                int32_t* r = p.gather.data() + 4 * k;
+                r[0] = head[k]; r[1] = steps[k]; r[2] = head[m]; r[3] = steps[m];
+            }
         }
     }
 

@@ -83,6 +83,7 @@ struct HostPlan {
     std::vector<float> tw4_hi, tw4_lo;      // four-step twiddles
     std::vector<int32_t> owner;             // per bin k = 0..L: first band | count << 24
     std::vector<int32_t> gather;            // per bin k = 0..L: covering bands of k and of L - k (see plan.cpp)
+    bool gather_wide = false;               // 32-byte records with absolute indices (see plan.cpp)
     std::vector<int32_t> bandbase;          // per band: off - k_lo
     std::vector<BandDev> banddev;
     std::vector<float> chirp, kern;         // Bluestein tables

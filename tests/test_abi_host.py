@@ -379,3 +379,12 @@ def test_sliced_band_list_plan(lib):
     assert lib.nsgcqt_sliced_plan_create_bands_host(ctypes.byref(h), fs, N + 2, 8, len(specs), arr) == nb.EINVAL
     assert not h.value
 
+
+def test_coarse_layouts_of_long_signals_build(lib):
+    # bands of a coarse layout over a long signal overlap by more than 2^15
+    # coefficients; the plan switches to wide overlap-add records
+    for args in [(48000.0, 20.0, 24000.0, 12, 2880000), (44100.0, 30.0, 22050.0, 12, 1323000)]:
+        lay = oracle.build_layout(*args)
+        p = nb.Plan(*args, 1, device=False)
+        assert p.n_coeffs == lay.n_coeffs
+

@@ -465,6 +465,38 @@ def test_concurrent_calls_from_threads():
         assert np.array_equal(to_np(outs[i]).view(np.uint32), refs[i].view(np.uint32)), i
 
 
+def test_coarse_long_layout_wide_records():
+    # 30 s at 44.1 kHz and 12 bins per octave: bands overlapping by more than
+    # 2^15 coefficients, which the overlap-add reads through 32-byte records
+    fs, fmin, fmax, B, N, b = 44100.0, 30.0, 22050.0, 12, 1323000, 2
+    lay = oracle.build_layout(fs, fmin, fmax, B, N)
+    p = nb.Plan(fs, fmin, fmax, B, N, b)
+    x = workloads.white(1323, b, N)
+    c = p.analyse(to_gpu(x))
+    assert oracle.rel_l2(to_np(c), oracle.analyse(lay, x, mode="fft")).max() <= REL_TOL
+    assert oracle.snr_db(x, to_np(p.synthesise(c))).min() >= SNR_MIN
+    y = workloads.coeff_cotangent(1324, b, p.n_coeffs)
+    assert oracle.rel_l2(to_np(p.synthesise(to_gpu(y))), oracle.synthesise(lay, y, mode="fft")).max() <= REL_TOL
+    ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
+    assert oracle.rel_l2(ta, oracle.adjoint_analysis(lay, y, mode="fft")).max() <= REL_TOL
+
+
+def test_maximum_huge_transform():
+    # N = 2^24: a DC band zero-padded to 2^24 points (the largest four-step
+    # band transform, 4096 x 4096) and a 2^22-point Nyquist band; both
+    # sidebands taper over two bins, which the middle band covers
+    N = 1 << 24
+    h = N // 4
+    specs = [(nb.BAND_DC, float(h), 2.0, 1 << 24), (nb.BAND_POSITIVE, float(h), 2.0, 0),
+             (nb.BAND_NYQUIST, float(h), 2.0, 0)]
+    lay = oracle.build_band_layout(48000.0, N, specs)
+    p = nb.Plan.from_bands(48000.0, N, specs, batch=1)
+    x = workloads.white(1 << 24, 1, N)
+    c = p.analyse(to_gpu(x))
+    assert oracle.rel_l2(to_np(c), oracle.analyse(lay, x, mode="fft")).max() <= REL_TOL
+    assert oracle.snr_db(x, to_np(p.synthesise(c))).min() >= SNR_MIN
+
+
 def test_workspace_too_small_raises():
     w = workloads.WORKLOADS["tiny"]
     p = nb.Plan(*w.plan_args, batch=1)
