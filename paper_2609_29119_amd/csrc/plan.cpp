@@ -37,20 +37,40 @@ int smallest_prime_factor(int64_t n) {
 
 // Forward DFT (eq. 1) of a smooth length in fp64, recursive decimation in
 // time. Used only at plan time for the Bluestein kernels.
-void host_dft(std::vector<cd>& x) {
+// Decimation in time by the smallest prime factor of n; w holds
+// omega_N^t for t < N, and a length-n subproblem uses its every (N/n)-th entry.
+void dft_rec(std::vector<cd>& x, const std::vector<cd>& w) {
     const int64_t n = static_cast<int64_t>(x.size());
     if (n <= 1) return;
+    const int64_t N = static_cast<int64_t>(w.size()), step = N / n;
     const int p = smallest_prime_factor(n);
     const int64_t m = n / p;
     std::vector<std::vector<cd>> sub(p, std::vector<cd>(m));
     for (int64_t j = 0; j < m; ++j)
         for (int r = 0; r < p; ++r) sub[r][j] = x[j * p + r];
-    for (int r = 0; r < p; ++r) host_dft(sub[r]);
-    for (int64_t k = 0; k < n; ++k) {
-        cd acc = 0.0;
-        for (int r = 0; r < p; ++r) acc += sub[r][k % m] * root(static_cast<int64_t>(r) * k, n);
-        x[k] = acc;
+    for (int r = 0; r < p; ++r) dft_rec(sub[r], w);
+    // X_k = sum_r omega_n^{r k} S_r[k mod m], k = q m + j; e tracks r k mod n
+    std::fill(x.begin(), x.end(), cd(0.0, 0.0));
+    for (int r = 0; r < p; ++r) {
+        const std::vector<cd>& sr = sub[r];
+        int64_t e = 0;
+        for (int64_t q = 0, k = 0; q < p; ++q)
+            for (int64_t j = 0; j < m; ++j, ++k) {
+                x[k] += sr[j] * w[e * step];
+                e += r;
+                if (e >= n) e -= n;
+            }
     }
+}
+
+// In-place DFT in fp64 (mixed radix; the roots are computed once, each with
+// its angle reduced exactly).
+void host_dft(std::vector<cd>& x) {
+    const int64_t n = static_cast<int64_t>(x.size());
+    if (n <= 1) return;
+    std::vector<cd> w(n);
+    for (int64_t t = 0; t < n; ++t) w[t] = root(t, n);
+    dft_rec(x, w);
 }
 
 void push_c(std::vector<float>& v, cd z) {
