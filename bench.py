@@ -76,9 +76,9 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def traffic_from_profiles(workload, kernel):
-    """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel sources; otherwise None."""
+def profile_traffic(workload):
+    """{stage: HBM bytes per launch} from the committed counter summary, if it
+    was taken on the current kernel sources; otherwise None."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
@@ -86,8 +86,22 @@ def traffic_from_profiles(workload, kernel):
         d = json.load(f)
     if d.get("source_hash") != kernel_source_hash():
         return None
-    k = d.get("kernels", {}).get(kernel)
-    return None if k is None else k.get("hbm_bytes_per_launch")
+    return {k: v.get("hbm_bytes_per_launch") for k, v in d.get("kernels", {}).items()}
+
+
+def traffic_from_profiles(workload, kernel):
+    """HBM bytes per launch of one kernel (see profile_traffic), or None."""
+    t = profile_traffic(workload)
+    return None if t is None else t.get(kernel)
+
+
+def counted_step_bytes(workload, kernels):
+    """Counted HBM bytes of one step: the sum over its launches, or None when
+    the summary is stale or misses one of them."""
+    t = profile_traffic(workload)
+    if t is None or any(t.get(k) is None for k in kernels):
+        return None
+    return float(sum(t[k] for k in kernels))
 
 
 def make_plan(w, batch):
@@ -105,11 +119,16 @@ def describe(w, b, N):
             f"{w.bins_per_octave} bins/oct")
 
 
-def cpu_baseline(w, x, target_s=12.0):
+def cpu_baseline(w, x, target_s=12.0, gpu_c=None, gpu_x=None):
     """The fp64 oracle's round trip (analysis + synthesis) timed on a bounded
     sample of the workload: signal counts double until one run reaches the
     whole batch or target_s seconds; whole-batch passes then repeat until
-    about target_s seconds of CPU work have been timed in total."""
+    about target_s seconds of CPU work have been timed in total.
+
+    With the GPU's coefficients and round-trip signals of the same inputs
+    (gpu_c [b][C] complex, gpu_x [b][N]), the last untimed-over result also
+    gives their relative L2 error against the oracle on the sampled signals,
+    max over the signals."""
     import oracle
     from threadpoolctl import threadpool_info
     if w.layout == "table1":
@@ -119,7 +138,8 @@ def cpu_baseline(w, x, target_s=12.0):
     k = 1
     while True:
         t0 = time.perf_counter()
-        oracle.synthesise(lay, oracle.analyse(lay, x[:k]))
+        c_ref = oracle.analyse(lay, x[:k])
+        x_ref = oracle.synthesise(lay, c_ref)
         dt = time.perf_counter() - t0
         if dt >= target_s or k >= x.shape[0]:
             break
@@ -127,15 +147,21 @@ def cpu_baseline(w, x, target_s=12.0):
     passes, total = 1, dt
     while total < target_s:
         t0 = time.perf_counter()
-        oracle.synthesise(lay, oracle.analyse(lay, x[:k]))
+        c_ref = oracle.analyse(lay, x[:k])
+        x_ref = oracle.synthesise(lay, c_ref)
         total += time.perf_counter() - t0
         passes += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": passes * k * w.n_samples / total, "unit": "samples/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"{passes} pass(es) over {k} of {x.shape[0]} signals, fp64 direct band DFTs, "
-                      f"analysis+synthesis, {total:.1f} s",
-            "host_cpus": len(os.sched_getaffinity(0))}
+    out = {"value": passes * k * w.n_samples / total, "unit": "samples/s", "cores": int(threads),
+           "kind": "oracle",
+           "sample": f"{passes} pass(es) over {k} of {x.shape[0]} signals, fp64 direct band DFTs, "
+                     f"analysis+synthesis, {total:.1f} s",
+           "host_cpus": len(os.sched_getaffinity(0))}
+    if gpu_c is not None and gpu_x is not None:
+        out["parity"] = {"signals": k,
+                         "coeffs_rel_l2_max": float(oracle.rel_l2(gpu_c[:k], c_ref).max()),
+                         "roundtrip_rel_l2_max": float(oracle.rel_l2(gpu_x[:k], x_ref).max())}
+    return out
 
 
 # HIP kernel (rocprofv3 name) -> stage name reported by nsgcqt_stage_info
@@ -390,6 +416,8 @@ def main():
                    "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": C},
         "pct_hbm_peak": 100.0 * b_alg / (ms * 1e-3) / HBM_PEAK,
         "alg_bytes_per_step": b_alg,
+        # x and c only, without the packed spectrum staged between the passes
+        "pct_hbm_peak_bmin": 100.0 * (8.0 * N + 16.0 * C) * b / (ms * 1e-3) / HBM_PEAK,
         "snr_db_min": float(snr.min()),
         "graph_replay_ms_per_step": graph_ms,
         "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_synthesise) / b,
@@ -401,8 +429,11 @@ def main():
                            "frac": achieved / (HBM_PEAK / 1e9),
                            "traffic": traffic_from_profiles(w.name, names[dom]) if b == w.batch else None}
         out["stages"] = stages
+        counted = counted_step_bytes(w.name, names) if b == w.batch else None
+        out["counted_bytes_per_step"] = counted
+        out["pct_hbm_peak_counted"] = None if counted is None else 100.0 * counted / (ms * 1e-3) / HBM_PEAK
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, x_np)
+        out["cpu_baseline"] = cpu_baseline(w, x_np, gpu_c=c.cpu().numpy(), gpu_x=xr_np)
     print(json.dumps(out), flush=True)
 
 

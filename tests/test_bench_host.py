@@ -45,3 +45,33 @@ def test_traffic_is_null_for_other_sources(tmp_path, monkeypatch):
     (prof / "traffic_x.json").write_text(json.dumps(
         {"source_hash": current, "kernels": {"k": {"hbm_bytes_per_launch": 5.0}}}))
     assert bench.traffic_from_profiles("x", "k") == 5.0
+
+
+def test_counted_step_bytes_sums_every_launch(tmp_path, monkeypatch):
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / "traffic_x.json").write_text(json.dumps(
+        {"source_hash": "h", "kernels": {"a": {"hbm_bytes_per_launch": 2.0},
+                                         "b": {"hbm_bytes_per_launch": 3.0}}}))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "h")
+    assert bench.counted_step_bytes("x", ["a", "b", "a"]) == 7.0
+    # a launch without counters makes the step figure unknown
+    assert bench.counted_step_bytes("x", ["a", "c"]) is None
+
+
+def test_cpu_baseline_reports_parity_of_the_given_outputs():
+    # the oracle leg compares the outputs it is handed with its own; a
+    # perturbed copy of the oracle's result shows up at the planted size
+    import numpy as np
+    import oracle
+    import workloads
+    w = workloads.WORKLOADS["tiny"]
+    x = np.random.default_rng(0).standard_normal((1, w.n_samples)).astype(np.float32)
+    lay = oracle.build_layout(*w.plan_args)
+    c = oracle.analyse(lay, x)
+    xr = oracle.synthesise(lay, c)
+    r = bench.cpu_baseline(w, x, target_s=0.01, gpu_c=c * (1 + 1e-3), gpu_x=xr)
+    assert r["kind"] == "oracle" and r["parity"]["signals"] == 1
+    assert abs(r["parity"]["coeffs_rel_l2_max"] - 1e-3) < 1e-9
+    assert r["parity"]["roundtrip_rel_l2_max"] < 1e-12
