@@ -291,15 +291,16 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan plan, const float* coeffs, int64_t n, f
 
 /* Profiling hook. While `events` is non-NULL, every compute call on this
  * plan brackets its i-th kernel launch with events[2i] (before) and
- * events[2i+1] (after), both recorded on the call's stream, for as many
- * pairs as given (hipEvent_t handles created by the caller; NULL entries
- * are skipped, so single kernels can be timed alone). The kernel order is
- * that of nsgcqt_stage_info. A NULL `events` stops recording. The setting
+ * events[2i+1] (after), both recorded on the stream the kernel runs on
+ * (the call's stream, or a plan side stream when the call's band phase
+ * fans out), for as many pairs as given (hipEvent_t handles created by the
+ * caller; NULL entries are skipped, so single kernels can be timed alone).
+ * The kernel order is that of nsgcqt_stage_info. A NULL `events` stops recording. The setting
  * is plan state: do not combine it with concurrent calls on the same plan. */
 int nsgcqt_set_stage_events(nsgcqt_plan plan, void* const* events, int n_events);
 
-/* Kernels one call of `op` enqueues (non-sliced plans): returns their
- * count (>= 0) or a negative status. For i in range, writes the kernel's
+/* Kernels one call of `op` enqueues (non-sliced plans), in enqueue order:
+ * returns their count (>= 0) or a negative status. For i in range, writes the kernel's
  * name and the algorithmic bytes one launch must move (inputs read once,
  * outputs written once; persistent tables excluded). name/alg_bytes may be
  * NULL. */

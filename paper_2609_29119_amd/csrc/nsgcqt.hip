@@ -60,9 +60,11 @@ struct nsgcqt_plan_s {
     hipEvent_t fork_ev = nullptr;
     hipEvent_t join_ev[kSide] = {};
     // only for plans whose band launches are all small and whose band phase
-    // is long (see upload)
+    // is long (see schedule)
     bool fan = false;
-    std::vector<int> lane;   // stream of each launch unit (buckets, then the huge-band chain): 0 = caller's
+    // launch units: the buckets, then the huge-band chain (when there are huge bands)
+    std::vector<int> lane;    // stream of each unit: 0 = caller's
+    std::vector<int> order;   // enqueue order of the units
     // the enqueue state above (events, the resident-block cache, the fork and
     // join events) is used by one call at a time
     std::mutex mu;
@@ -140,36 +142,40 @@ int upload(nsgcqt_plan_s* p) {
         HIP_TRY(hipEventCreateWithFlags(&p->join_ev[i], evf));
     }
     HIP_TRY(hipEventCreateWithFlags(&p->fork_ev, evf));
-    // overlap pays when no band launch fills the GPU by itself and the band
-    // phase is long against the fork and join (~25 us each way): at least
-    // 6M element slots of band work
-    int most = 0;
-    double work = 4.0 * static_cast<double>(h.Hn) * static_cast<double>(h.batch);
-    for (const auto& bk : h.buckets) {
-        most = std::max(most, bk.nitems);
-        work += static_cast<double>(bk.nitems) * bk.nt * bk.ept;
-    }
-    p->fan = most < 2048 && work >= 6e6;
-    // longest first onto the least loaded of the four streams
-    {
-        std::vector<double> cost;
-        for (const auto& bk : h.buckets) cost.push_back(static_cast<double>(bk.nitems) * bk.nt * bk.ept);
-        cost.push_back(4.0 * static_cast<double>(h.Hn) * static_cast<double>(h.batch));
-        std::vector<int> order(cost.size());
-        for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int>(i);
-        std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cost[a] > cost[b]; });
-        double load[nsgcqt_plan_s::kSide + 1] = {};
-        p->lane.assign(cost.size(), 0);
-        for (int u : order) {
-            int best = 0;
-            for (int k = 1; k <= nsgcqt_plan_s::kSide; ++k)
-                if (load[k] < load[best]) best = k;
-            p->lane[u] = best;
-            load[best] += cost[u];
-        }
-    }
     p->device = true;
     return NSGCQT_OK;
+}
+
+// Launch schedule of the band phase, from the host plan alone. Overlap pays
+// when no band launch fills the GPU by itself and the band phase is long
+// against the fork and join (~25 us each way): at least 6M element slots of
+// band work. Then units are enqueued longest first, each onto the least
+// loaded of the four streams; otherwise in bucket order on the caller's.
+void schedule(nsgcqt_plan_s* p) {
+    const HostPlan& h = p->h;
+    std::vector<double> cost;
+    int most = 0;
+    for (const auto& bk : h.buckets) {
+        most = std::max(most, bk.nitems);
+        cost.push_back(static_cast<double>(bk.nitems) * bk.nt * bk.ept);
+    }
+    if (!h.bigs.empty()) cost.push_back(4.0 * static_cast<double>(h.Hn) * static_cast<double>(h.batch));
+    double work = 0.0;
+    for (double c : cost) work += c;
+    p->fan = most < 2048 && work >= 6e6;
+    p->order.resize(cost.size());
+    for (size_t i = 0; i < cost.size(); ++i) p->order[i] = static_cast<int>(i);
+    p->lane.assign(cost.size(), 0);
+    if (!p->fan) return;
+    std::stable_sort(p->order.begin(), p->order.end(), [&](int a, int b) { return cost[a] > cost[b]; });
+    double load[nsgcqt_plan_s::kSide + 1] = {};
+    for (int u : p->order) {
+        int best = 0;
+        for (int k = 1; k <= nsgcqt_plan_s::kSide; ++k)
+            if (load[k] < load[best]) best = k;
+        p->lane[u] = best;
+        load[best] += cost[u];
+    }
 }
 
 // Releases the plan's device tables, side streams and events.
@@ -199,15 +205,19 @@ struct Fanout {
     hipStream_t s;
     bool forked = false;
     bool used[nsgcqt_plan_s::kSide] = {};
+    // the fork point precedes every launch of the phase, including those
+    // that go on s itself
+    int begin() {
+        if (!p->fan) return NSGCQT_OK;
+        HIP_TRY(hipEventRecord(p->fork_ev, s));
+        forked = true;
+        return NSGCQT_OK;
+    }
     int stream(int u, hipStream_t* out) {
         const int k = p->fan ? p->lane[u] : 0;
-        if (k == 0) {
+        if (k == 0 || !forked) {
             *out = s;
             return NSGCQT_OK;
-        }
-        if (!forked) {
-            HIP_TRY(hipEventRecord(p->fork_ev, s));
-            forked = true;
         }
         if (!used[k - 1]) {
             HIP_TRY(hipStreamWaitEvent(p->side[k - 1], p->fork_ev, 0));
@@ -227,11 +237,21 @@ struct Fanout {
 };
 
 // ---------------------------------------------------------------- launches
+// Kernels with more than 64 KB of dynamic LDS get the attribute that allows
+// it, once per kernel and device at the largest size asked for so far.
 template <typename K>
 int launch_prep(K kernel, int lds_bytes) {
-    if (lds_bytes > 64 * 1024)
-        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes));
+    if (lds_bytes <= 64 * 1024) return NSGCQT_OK;
+    static std::mutex mu;
+    static std::map<std::pair<const void*, int>, int> done;
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    const auto key = std::make_pair(reinterpret_cast<const void*>(kernel), dev);
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = done.find(key);
+    if (it != done.end() && it->second >= lds_bytes) return NSGCQT_OK;
+    HIP_TRY(hipFuncSetAttribute(key.first, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes));
+    done[key] = lds_bytes;
     return NSGCQT_OK;
 }
 
@@ -374,39 +394,34 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
 // The band tiers, one launch each.
 // Analysis reads the router factors rt, synthesis the weights wt.
 // Bucket i runs as fanout unit i.
-int run_bands(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float4* rt, const float* wt,
-              int batch, Fanout& fan) {
+int run_bucket(nsgcqt_plan_s* p, size_t bi, bool analysis, const float2* in, float2* out, const float4* rt,
+               const float* wt, int batch, Fanout& fan) {
     const HostPlan& h = p->h;
-    for (size_t bi = 0; bi < h.buckets.size(); ++bi) {
-        const Bucket& bk = h.buckets[bi];
-        hipStream_t s;
-        if (int r = fan.stream(static_cast<int>(bi), &s)) return r;
-        const int lds = bk.lds_elems * static_cast<int>(sizeof(float2));
-        const dim3 grid(bk.nitems), block(bk.nt);
-        auto go = [&](auto ka, auto ks) -> int {
-            ev_start(p, s);
-            if (analysis) {
-                if (int r = launch_prep(ka, lds)) return r;
-                hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, rt, p->T, bk.item_off, bk.nitems, batch,
-                                   static_cast<int>(h.L), static_cast<long long>(h.C));
-            } else {
-                if (int r = launch_prep(ks, lds)) return r;
-                hipLaunchKernelGGL(ks, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
-                                   static_cast<long long>(h.C));
-            }
-            HIP_TRY(hipGetLastError());
-            ev_end(p, s);
-            return NSGCQT_OK;
-        };
-        int r = NSGCQT_OK;
-        if (bk.nt == 64) r = go(k_band_analysis<64, 8>, k_band_synthesis<64, 8>);
-        else if (bk.nt == 256 && bk.ept == 8) r = go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
-        else if (bk.nt == 256) r = go(k_band_analysis<256, 16>, k_band_synthesis<256, 16>);
-        else if (bk.nt == 512) r = go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
-        else r = go(k_band_analysis<1024, 16>, k_band_synthesis<1024, 16>);
-        if (r) return r;
-    }
-    return NSGCQT_OK;
+    const Bucket& bk = h.buckets[bi];
+    hipStream_t s;
+    if (int r = fan.stream(static_cast<int>(bi), &s)) return r;
+    const int lds = bk.lds_elems * static_cast<int>(sizeof(float2));
+    const dim3 grid(bk.nitems), block(bk.nt);
+    auto go = [&](auto ka, auto ks) -> int {
+        ev_start(p, s);
+        if (analysis) {
+            if (int r = launch_prep(ka, lds)) return r;
+            hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, rt, p->T, bk.item_off, bk.nitems, batch,
+                               static_cast<int>(h.L), static_cast<long long>(h.C));
+        } else {
+            if (int r = launch_prep(ks, lds)) return r;
+            hipLaunchKernelGGL(ks, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
+                               static_cast<long long>(h.C));
+        }
+        HIP_TRY(hipGetLastError());
+        ev_end(p, s);
+        return NSGCQT_OK;
+    };
+    if (bk.nt == 64) return go(k_band_analysis<64, 8>, k_band_synthesis<64, 8>);
+    if (bk.nt == 256 && bk.ept == 8) return go(k_band_analysis<256, 8>, k_band_synthesis<256, 8>);
+    if (bk.nt == 256) return go(k_band_analysis<256, 16>, k_band_synthesis<256, 16>);
+    if (bk.nt == 512) return go(k_band_analysis<512, 16>, k_band_synthesis<512, 16>);
+    return go(k_band_analysis<1024, 16>, k_band_synthesis<1024, 16>);
 }
 
 // Huge bands: column pass and row pass over every huge band, then for the
@@ -447,6 +462,25 @@ BigArgs big_args(nsgcqt_plan_s* p, char* ws, int64_t hoff, int batch, bool analy
     return a;
 }
 
+// The band phase of one call: every bucket and the huge-band chain, in the
+// plan's schedule order and on its streams; returns with s after all of them.
+int run_band_phase(nsgcqt_plan_s* p, bool analysis, const float2* in, float2* out, const float4* rt,
+                   const float* wt, BigArgs a, int batch, hipStream_t s) {
+    const HostPlan& h = p->h;
+    Fanout fan{p, s};
+    if (int r = fan.begin()) return r;
+    for (int u : p->order) {
+        if (u < static_cast<int>(h.buckets.size())) {
+            if (int r = run_bucket(p, static_cast<size_t>(u), analysis, in, out, rt, wt, batch, fan)) return r;
+        } else {
+            hipStream_t sb;
+            if (int r = fan.stream(u, &sb)) return r;
+            if (int r = run_big(p, a, batch, sb)) return r;
+        }
+    }
+    return fan.join();
+}
+
 // Analysis chain (T, or S^dagger with its weights) for `batch` signals or slices.
 int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float4* rt, int batch, SliceIn sl,
                   char* ws, hipStream_t s) {
@@ -455,18 +489,12 @@ int chain_analyse(nsgcqt_plan_s* p, const float* x, float2* coeffs, const float4
     float2* Z = reinterpret_cast<float2*>(ws + align256(8 * h.L * batch));
     if (int r = run_fwd_a(p, x, Y, batch, sl, static_cast<long long>(h.N), s)) return r;
     if (int r = run_pass_b<false>(p, Y, Z, batch, static_cast<long long>(h.L), s)) return r;
-    Fanout fan{p, s};
-    if (int r = run_bands(p, true, Z, coeffs, rt, nullptr, batch, fan)) return r;
     BigArgs a = big_args(p, ws, h.off_h_an, h.spc ? h.spc : batch, true);
     a.Z = Z;
     a.cout = coeffs;
     a.rt = rt;
-    if (!h.bigs.empty()) {
-        hipStream_t sb;
-        if (int r = fan.stream(static_cast<int>(h.buckets.size()), &sb)) return r;
-        if (int r = run_big(p, a, batch, sb)) return r;
-    }
-    return fan.join();
+    if (int r = run_band_phase(p, true, Z, coeffs, rt, nullptr, a, batch, s)) return r;
+    return NSGCQT_OK;
 }
 
 // Synthesis chain (S, or T^dagger with its weights); output is [batch][N] f32.
@@ -475,18 +503,11 @@ int chain_synthesise(nsgcqt_plan_s* p, const float2* coeffs, float* xo, const fl
     const HostPlan& h = p->h;
     float2* W = reinterpret_cast<float2*>(ws);
     float2* Y = reinterpret_cast<float2*>(ws + align256(8 * h.C * batch));
-    Fanout fan{p, s};
-    if (int r = run_bands(p, false, coeffs, W, nullptr, wt, batch, fan)) return r;
     BigArgs a = big_args(p, ws, h.off_h_syn, h.spc ? h.spc : batch, false);
     a.cin = coeffs;
     a.W = W;
     a.wt = wt;
-    if (!h.bigs.empty()) {
-        hipStream_t sb;
-        if (int r = fan.stream(static_cast<int>(h.buckets.size()), &sb)) return r;
-        if (int r = run_big(p, a, batch, sb)) return r;
-    }
-    if (int r = fan.join()) return r;
+    if (int r = run_band_phase(p, false, coeffs, W, nullptr, wt, a, batch, s)) return r;
     if (int r = run_inv_a(p, W, Y, batch, s)) return r;
     return run_pass_b<true>(p, Y, reinterpret_cast<float2*>(xo), batch, static_cast<long long>(h.L), s);
 }
@@ -528,6 +549,7 @@ int create(nsgcqt_plan* out, bool device, Build build) {
         delete p;
         return set_err(r, err);
     }
+    schedule(p);
     if (device) {
         r = upload(p);
         if (r != NSGCQT_OK) {
@@ -814,11 +836,6 @@ int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, doub
     if (an) {
         st.push_back({"fft_fwd_a", 16.0 * L * b});
         st.push_back({"fft_fwd_b", 16.0 * L * b});
-        for (const auto& bk : h.buckets) {
-            const double cb = static_cast<double>(bk.coeffs);
-            st.push_back({"band_analysis_" + std::to_string(bk.nt) + "x" + std::to_string(bk.ept),
-                          (cb / C * 8.0 * L + 8.0 * cb) * b});
-        }
     }
     // huge-band passes: the column pass reads its input share and writes the
     // intermediate, the row pass reads it and writes the output or the
@@ -835,13 +852,19 @@ int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, doub
             big.push_back({an ? "big_analysis_b2" : "big_synthesis_b2", (8.0 * hb + 8.0 * cbb) * b});
         }
     }
-    if (an) {
-        st.insert(st.end(), big.begin(), big.end());
-    } else {
-        for (const auto& bk : h.buckets)
-            st.push_back({"band_synthesis_" + std::to_string(bk.nt) + "x" + std::to_string(bk.ept),
-                          16.0 * static_cast<double>(bk.coeffs) * b});
-        st.insert(st.end(), big.begin(), big.end());
+    // the band phase in launch order
+    for (int u : p->order) {
+        if (u == static_cast<int>(h.buckets.size())) {
+            st.insert(st.end(), big.begin(), big.end());
+            continue;
+        }
+        const Bucket& bk = h.buckets[u];
+        const double cb = static_cast<double>(bk.coeffs);
+        const std::string shape = std::to_string(bk.nt) + "x" + std::to_string(bk.ept);
+        if (an) st.push_back({"band_analysis_" + shape, (cb / C * 8.0 * L + 8.0 * cb) * b});
+        else st.push_back({"band_synthesis_" + shape, 16.0 * cb * b});
+    }
+    if (!an) {
         st.push_back({"fft_inv_a_overlap_add", (8.0 * C + 8.0 * L) * b});
         st.push_back({"fft_inv_b", 16.0 * L * b});
     }

@@ -388,3 +388,17 @@ def test_coarse_layouts_of_long_signals_build(lib):
         p = nb.Plan(*args, 1, device=False)
         assert p.n_coeffs == lay.n_coeffs
 
+
+
+def test_stage_order_follows_the_launch_schedule(lib):
+    # band phases that fill the GPU launch by bucket in ascending transform
+    # size; phases of small launches with enough work fan out and are
+    # enqueued longest first
+    stress = [n for n, _ in _host_plan(workloads.WORKLOADS["stress"]).stage_info(nb.OP_ANALYSE)]
+    assert stress[2:] == ["band_analysis_64x8", "band_analysis_256x8", "band_analysis_256x16"]
+    train = _host_plan(workloads.WORKLOADS["train"])
+    an = [n for n, _ in train.stage_info(nb.OP_ANALYSE)]
+    assert an[2:] == ["band_analysis_1024x16", "band_analysis_512x16", "band_analysis_256x16",
+                      "band_analysis_256x8", "band_analysis_64x8"]
+    syn = [n for n, _ in train.stage_info(nb.OP_SYNTHESISE)]
+    assert syn == [n.replace("analysis", "synthesis") for n in an[2:]] + ["fft_inv_a_overlap_add", "fft_inv_b"]
