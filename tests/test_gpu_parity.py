@@ -300,6 +300,10 @@ BAND_LISTS = [
     # Bluestein and a Nyquist band of 9000, all through the huge-band path
     ("huge_N4000", 4000, [10.0 * 1.4 ** j for j in range(14)],
      [0, 0, 0, 0, 0, 0, 8200, 0, 0, 8209, 0, 0, 0, 0], 0, 9000, 2, "fft"),
+    # transform lengths on both sides of every band-kernel tier limit (512,
+    # 2048, 4096, 8192, 16384) and of the huge-band path
+    ("tier_edges_N4000", 4000, [10.0 * 1.4 ** j for j in range(14)],
+     [512, 513, 2048, 2050, 4096, 4100, 8192, 8200, 16384, 16400, 0, 0, 0, 0], 0, 0, 2, "fft"),
 ]
 
 
@@ -310,6 +314,10 @@ def test_band_list_against_oracle(case):
     lay = oracle.build_band_layout(float(N), N, specs)
     p = nb.Plan.from_bands(float(N), N, specs, batch=b)
     assert any(bd.length > bd.k_hi - bd.k_lo + 1 for bd in p.bands())
+    if name.startswith("tier_edges"):
+        kinds = {n for n, _ in p.stage_info(nb.OP_ANALYSE)}
+        assert {"band_analysis_64x8", "band_analysis_256x8", "band_analysis_256x16", "band_analysis_512x16",
+                "band_analysis_1024x16", "big_analysis_a"} <= kinds
     x = workloads.white(N + 5, b, N)
     y = workloads.coeff_cotangent(N + 6, b, p.n_coeffs)
     xs_ = workloads.signal_cotangent(N + 7, b, N)
