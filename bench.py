@@ -67,12 +67,43 @@ class HipEvents:
             self.rt.hipEventDestroy(ctypes.c_void_p(e))
 
 
+def strip_c_comments(text):
+    """C/C++ source without its comments and with runs of whitespace
+    collapsed, so that edits to comments or layout keep the same hash.
+    String and character literals are kept as they are."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_hash():
+    """Hash of the library's C++/HIP sources (kernels, launches and plan
+    building), comments and whitespace excluded: stored counter summaries
+    are reported only while it matches."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_29119_amd", "csrc")
     for f in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(fh.read())
+        if not f.endswith((".hip", ".hpp", ".cpp", ".h")):
+            continue
+        with open(os.path.join(csrc, f), encoding="utf-8") as fh:
+            h.update(f.encode() + b"\0" + strip_c_comments(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

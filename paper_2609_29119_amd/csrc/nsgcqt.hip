@@ -391,9 +391,8 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
     return NSGCQT_OK;
 }
 
-// The band tiers, one launch each.
+// One band tier (bucket bi) as one launch, on the stream of fan-out unit bi.
 // Analysis reads the router factors rt, synthesis the weights wt.
-// Bucket i runs as fanout unit i.
 int run_bucket(nsgcqt_plan_s* p, size_t bi, bool analysis, const float2* in, float2* out, const float4* rt,
                const float* wt, int batch, Fanout& fan) {
     const HostPlan& h = p->h;

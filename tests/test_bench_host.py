@@ -75,3 +75,12 @@ def test_cpu_baseline_reports_parity_of_the_given_outputs():
     assert r["kind"] == "oracle" and r["parity"]["signals"] == 1
     assert abs(r["parity"]["coeffs_rel_l2_max"] - 1e-3) < 1e-9
     assert r["parity"]["roundtrip_rel_l2_max"] < 1e-12
+
+
+def test_source_hash_ignores_comments_and_layout():
+    a = 'int f(int x) { return x + 1; } // one\nconst char* s = "a // b";'
+    b = '/* doc */\nint f(int x) {\n    return x + 1;   // plus one\n}\nconst char* s = "a // b";'
+    assert bench.strip_c_comments(a) == bench.strip_c_comments(b)
+    # code and string literals still count
+    assert bench.strip_c_comments(a) != bench.strip_c_comments(a.replace("+ 1", "+ 2"))
+    assert bench.strip_c_comments(a) != bench.strip_c_comments(a.replace('"a // b"', '"a // c"'))
