@@ -35,7 +35,10 @@ ERB-rate scale (another painless frame of the kind Sec. 6 says the
 construction extends to).
 
 Parity: pinned by tests (closed-form windows, sum h g = 1, coverage bounds,
-band counts, agreement with an independent integer layout).
+band counts, agreement with an independent integer layout). Two conventions
+are parity unpinned, since no passage fixes them: the phase of the slot map
+(which bin goes to slot 0; every injective map gives a valid transform), and
+the fan-out of the Table 1 reading, 6 against the paper's 7.
 """
 from __future__ import annotations
 
