@@ -385,6 +385,8 @@ def main():
     t_start = torch.cuda.Event(enable_timing=True)
     t_stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    mem0 = torch.cuda.memory_allocated()
     t0 = time.perf_counter()
     t_start.record()
     for i in range(K):
@@ -392,6 +394,7 @@ def main():
     t_stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    alloc_steps = torch.cuda.max_memory_allocated() - mem0
     plan.set_stage_events(None)
     gpu_ms = t_start.elapsed_time(t_stop)
     ms = max(gpu_ms, wall * 1e3) / K
@@ -452,6 +455,9 @@ def main():
         "snr_db_min": float(snr.min()),
         "graph_replay_ms_per_step": graph_ms,
         "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_synthesise) / b,
+        # allocator peak above what was live before the timed steps (the
+        # workspace and outputs are allocated beforehand)
+        "alloc_during_steps_bytes": alloc_steps,
     }
     if dom is not None:
         achieved = algb[dom] / (dom_ms * 1e-3) / 1e9
