@@ -305,7 +305,7 @@ def main():
                           args.copy_calib_mb * 1024 * 1024)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; a batch shards across GPUs with no "
+        print(json.dumps({"error": "the benchmark runs on one GPU; a batch shards across GPUs with no "
                           "communication, so --gpus must be 1"}))
         sys.exit(2)
 

@@ -79,7 +79,7 @@ typedef enum {
     NSGCQT_ENOMEM = -2,       /* device or host allocation failed at plan time */
     NSGCQT_EDEVICE = -3,      /* a HIP call failed; see nsgcqt_last_error() */
     NSGCQT_EWORKSPACE = -4,   /* ws_bytes below the size the plan requires */
-    NSGCQT_EUNSUPPORTED = -5  /* valid transform this build cannot evaluate */
+    NSGCQT_EUNSUPPORTED = -5  /* valid transform the library cannot evaluate */
 } nsgcqt_status;
 
 typedef enum {
