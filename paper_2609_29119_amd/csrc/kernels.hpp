@@ -114,6 +114,27 @@ __device__ __forceinline__ void load_tw4(float2* t4, const Pass& p, const Tables
         [&](int i, float2 v) { t4[i] = v; });
 }
 
+// The same table in two steps, so that its global reads can overlap other
+// reads: tw4_fetch issues the read of entry threadIdx.x into a register,
+// tw4_store writes it to LDS later and reads the entries from NT on directly.
+template <int NT>
+__device__ __forceinline__ float2 tw4_fetch(const Pass& p, const Tables& T) {
+    const int i = min(static_cast<int>(threadIdx.x), p.nhi4 + (1 << p.split) - 1);
+    return *(i < p.nhi4 ? T.tw4_hi + i : T.tw4_lo + (i - p.nhi4));
+}
+template <int NT>
+__device__ __forceinline__ void tw4_store(float2* t4, float2 v, const Pass& p, const Tables& T) {
+    const int n = p.nhi4 + (1 << p.split);
+    if (static_cast<int>(threadIdx.x) < n) t4[threadIdx.x] = v;
+    load_phase<NT, 2>(
+        n - NT,
+        [&](int j) {
+            const int i = j + NT;
+            return *(i < p.nhi4 ? T.tw4_hi + i : T.tw4_lo + (i - p.nhi4));
+        },
+        [&](int j, float2 w) { t4[j + NT] = w; });
+}
+
 __device__ __forceinline__ float2 tw4(const float2* t4, const Pass& p, int t) {
     return cmul(t4[t >> p.split], t4[p.nhi4 + (t & ((1 << p.split) - 1))]);
 }
@@ -261,7 +282,9 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
     extern __shared__ float2 lds[];
     float2 *t4, *buf;
     pass_lds(lds, p, true, t4, buf);
-    load_tw4<NT>(t4, p, T);
+    // the four-step twiddles are needed only by the final store: their reads
+    // go out first and land while the bin records are read
+    const float2 t4pre = tw4_fetch<NT>(p, T);
     const int G = p.ntile * batch;
     const int lid = xcd_remap(blockIdx.x, G);
     const int tile = lid % p.ntile, sig = lid / p.ntile;
@@ -317,6 +340,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_inv_a(const float2* __restrict__
             }
         }
     }
+    tw4_store<NT>(t4, t4pre, p, T);
     __syncthreads();
     lds_fft<NT, EPT>(buf, S, p.lgnb, T.ffts + p.fft, T.tw);
     __syncthreads();
