@@ -59,7 +59,10 @@
  * Errors
  *   Every function returns an nsgcqt_status. No C++ exception crosses the
  *   ABI. The text of the last error on the calling thread is returned by
- *   nsgcqt_last_error().
+ *   nsgcqt_last_error(). EDEVICE reports only the HIP calls the library
+ *   makes itself (each launch is checked by its own status): an error that
+ *   an earlier HIP call of the caller left on the thread is neither
+ *   reported nor cleared.
  */
 #ifndef NSGCQT_H
 #define NSGCQT_H

@@ -9,6 +9,9 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <tuple>
+#include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "../../include/nsgcqt.h"
@@ -31,6 +34,29 @@ int set_err(int code, const std::string& msg) {
         hipError_t e_ = (expr);                                                        \
         if (e_ != hipSuccess)                                                          \
             return set_err(NSGCQT_EDEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+// Launches kernel k with the arguments converted to its parameter types and
+// returns the status of this launch alone. (hipGetLastError after a launch
+// would also report an error that an earlier, unrelated HIP call of the
+// caller left on the thread.)
+template <typename... P, typename... A>
+hipError_t launch_kernel(void (*k)(P...), dim3 grid, dim3 block, size_t lds, hipStream_t s, A&&... a) {
+    static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
+    std::tuple<std::decay_t<P>...> vals(std::forward<A>(a)...);
+    return std::apply(
+        [&](auto&... v) {
+            void* args[] = {static_cast<void*>(&v)...};
+            return hipLaunchKernel(reinterpret_cast<const void*>(k), grid, block, args, lds, s);
+        },
+        vals);
+}
+
+#define LAUNCH_TRY(...)                                                                \
+    do {                                                                               \
+        hipError_t e_ = launch_kernel(__VA_ARGS__);                                    \
+        if (e_ != hipSuccess)                                                          \
+            return set_err(NSGCQT_EDEVICE, std::string("kernel launch: ") + hipGetErrorString(e_)); \
     } while (0)
 
 int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
@@ -330,8 +356,7 @@ int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl
         const int res = resident_blocks(p, k, p->h.fs4.nt_a, lds);
         const int grid = res > 0 ? std::min(tiles, res) : tiles;
         ev_start(p, s);
-        hipLaunchKernelGGL(k, dim3(grid), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch, sig_stride);
-        HIP_TRY(hipGetLastError());
+        LAUNCH_TRY(k, dim3(grid), dim3(p->h.fs4.nt_a), lds, s, x, Y, q, p->T, sl, batch, sig_stride);
         ev_end(p, s);
         return NSGCQT_OK;
     };
@@ -356,9 +381,8 @@ int run_inv_a(nsgcqt_plan_s* p, const float2* W, float2* Y, int batch, hipStream
     auto launch = [&](auto k) -> int {
         if (int r = launch_prep(k, lds)) return r;
         ev_start(p, s);
-        hipLaunchKernelGGL(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, W, Y, q, p->T, batch,
-                           static_cast<long long>(p->h.C));
-        HIP_TRY(hipGetLastError());
+        LAUNCH_TRY(k, dim3(q.ntile * batch), dim3(p->h.fs4.nt_a), lds, s, W, Y, q, p->T, batch,
+                   static_cast<long long>(p->h.C));
         ev_end(p, s);
         return NSGCQT_OK;
     };
@@ -381,9 +405,8 @@ int run_pass_b(nsgcqt_plan_s* p, const float2* Y, float2* out, int batch, long l
         const int res = resident_blocks(p, k, p->h.fs4.nt_b, lds);
         const int grid = res > 0 ? std::min(tiles, res) : tiles;
         ev_start(p, s);
-        hipLaunchKernelGGL(k, dim3(grid), dim3(p->h.fs4.nt_b), lds, s, Y, out, q, p->T, batch,
-                           out_stride, inv_L);
-        HIP_TRY(hipGetLastError());
+        LAUNCH_TRY(k, dim3(grid), dim3(p->h.fs4.nt_b), lds, s, Y, out, q, p->T, batch,
+                   out_stride, inv_L);
         ev_end(p, s);
         return NSGCQT_OK;
     };
@@ -405,14 +428,13 @@ int run_bucket(nsgcqt_plan_s* p, size_t bi, bool analysis, const float2* in, flo
         ev_start(p, s);
         if (analysis) {
             if (int r = launch_prep(ka, lds)) return r;
-            hipLaunchKernelGGL(ka, grid, block, lds, s, in, out, rt, p->T, bk.item_off, bk.nitems, batch,
-                               static_cast<int>(h.L), static_cast<long long>(h.C));
+            LAUNCH_TRY(ka, grid, block, lds, s, in, out, rt, p->T, bk.item_off, bk.nitems, batch,
+                       static_cast<int>(h.L), static_cast<long long>(h.C));
         } else {
             if (int r = launch_prep(ks, lds)) return r;
-            hipLaunchKernelGGL(ks, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
-                               static_cast<long long>(h.C));
+            LAUNCH_TRY(ks, grid, block, lds, s, in, out, wt, p->T, bk.item_off, bk.nitems, batch,
+                       static_cast<long long>(h.C));
         }
-        HIP_TRY(hipGetLastError());
         ev_end(p, s);
         return NSGCQT_OK;
     };
@@ -438,12 +460,11 @@ int run_big(nsgcqt_plan_s* p, BigArgs a, int batch, hipStream_t s) {
         if (n == 0) continue;
         ev_start(p, s);
         if (pass % 2 == 0)
-            hipLaunchKernelGGL(ka, dim3(n), dim3(512), h.big_lds_a, s, a, p->T, h.big_off[pass], n, batch,
-                               pass == 0 ? in0 : kBigInBlu2);
+            LAUNCH_TRY(ka, dim3(n), dim3(512), h.big_lds_a, s, a, p->T, h.big_off[pass], n, batch,
+                       pass == 0 ? in0 : kBigInBlu2);
         else
-            hipLaunchKernelGGL(kb, dim3(n), dim3(512), h.big_lds_b, s, a, p->T, h.big_off[pass], n, batch,
-                               pass == 3 ? 1 : 0);
-        HIP_TRY(hipGetLastError());
+            LAUNCH_TRY(kb, dim3(n), dim3(512), h.big_lds_b, s, a, p->T, h.big_off[pass], n, batch,
+                       pass == 3 ? 1 : 0);
         ev_end(p, s);
     }
     return NSGCQT_OK;
@@ -804,9 +825,8 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, floa
         const int64_t span = static_cast<int64_t>(cnt) * H;
         const int blocks = static_cast<int>(std::min<int64_t>((span + 255) / 256, 8192));
         ev_start(p, s);
-        hipLaunchKernelGGL(k_ola, dim3(blocks), dim3(256), 0, s, y, carry[flip], carry[flip ^ 1], xo,
-                           static_cast<int>(s0), cnt, static_cast<int>(h.N), static_cast<long long>(n));
-        HIP_TRY(hipGetLastError());
+        LAUNCH_TRY(k_ola, dim3(blocks), dim3(256), 0, s, y, carry[flip], carry[flip ^ 1], xo,
+                   static_cast<int>(s0), cnt, static_cast<int>(h.N), static_cast<long long>(n));
         ev_end(p, s);
         flip ^= 1;
     }

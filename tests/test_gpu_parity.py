@@ -438,6 +438,57 @@ def test_graph_capture_with_side_streams():
         assert np.array_equal(to_np(xr).view(np.uint32), xe.view(np.uint32)), i
 
 
+def test_stage_events_bracket_every_launch_with_side_streams():
+    # with the band phase fanned out over the side streams, the i-th event
+    # pair brackets the i-th kernel of nsgcqt_stage_info on the stream that
+    # kernel runs on: every pair is recorded and times a positive interval,
+    # the results are those of a call without events, and a pair beyond the
+    # listed kernels is never recorded. Querying that pair fails and leaves a
+    # HIP error on the thread, which the next library call must not report
+    # as its own.
+    import sys
+    import os
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import HipEvents
+    w = workloads.WORKLOADS["train"]
+    b, N = w.batch, w.n_samples
+    p = nb.Plan(*w.plan_args, batch=b)
+    na, ns = len(p.stage_info(nb.OP_ANALYSE)), len(p.stage_info(nb.OP_SYNTHESISE))
+    assert any(n.startswith("band_analysis_1024") for n, _ in p.stage_info(nb.OP_ANALYSE))
+    x = to_gpu(workloads.white(81, b, N))
+    ce = to_np(p.analyse(x))
+    xe = to_np(p.synthesise(to_gpu(ce)))
+    ev = HipEvents(2 * (na + 1) + 2 * (ns + 1))
+    try:
+        ea, es = ev.ev[:2 * (na + 1)], ev.ev[2 * (na + 1):]
+        p.set_stage_events(ea)
+        c = p.analyse(x)
+        p.set_stage_events(es)
+        xr = p.synthesise(c)
+        p.set_stage_events(None)
+        assert np.array_equal(to_np(c).view(np.uint32), ce.view(np.uint32))
+        assert np.array_equal(to_np(xr).view(np.uint32), xe.view(np.uint32))
+        # everything the library call below needs exists beforehand: while
+        # the error is pending, nothing but the library touches HIP (torch's
+        # own checks would report it)
+        c2 = torch.empty_like(c)
+        ws_a = p.workspace(nb.OP_ANALYSE)
+        cur = torch.cuda.current_stream()
+        torch.cuda.synchronize()
+        for evs, n in ((ea, na), (es, ns)):
+            for i in range(n):
+                assert ev.elapsed_ms(evs[2 * i], evs[2 * i + 1]) > 0.0, i
+            with pytest.raises(RuntimeError):
+                ev.elapsed_ms(evs[2 * n], evs[2 * n + 1])
+            p.analyse(x, out=c2, ws=ws_a, stream=cur)    # the error is still pending
+            assert ev.rt.hipGetLastError() != 0          # it was: clear it
+            assert np.array_equal(to_np(c2).view(np.uint32), ce.view(np.uint32))
+    finally:
+        p.set_stage_events(None)
+        ev.rt.hipGetLastError()
+        ev.close()
+
+
 def test_concurrent_calls_from_threads():
     # two host threads drive one plan (the training plan, whose calls fork
     # onto the plan's side streams) on their own streams and workspaces; every
