@@ -41,10 +41,13 @@
  * Pointers and ownership
  *   - x, coeffs, outputs and the workspace are device pointers owned by the
  *     caller. The workspace size comes from nsgcqt_plan_info(); the library
- *     never allocates during a compute call.
+ *     never allocates during a compute call. Coefficients, the workspace and
+ *     the signals of the non-sliced calls must be 8-byte aligned, the
+ *     signals of the sliced calls 4-byte aligned (EINVAL otherwise).
  *   - A plan owns its device tables (allocated on the device current at
- *     creation, freed by nsgcqt_plan_destroy). A plan's layout and tables
- *     are immutable. Calls on one plan from several host threads take turns
+ *     creation, freed by nsgcqt_plan_destroy). Compute calls must be made
+ *     with that device current; otherwise they return EINVAL and enqueue
+ *     nothing. A plan's layout and tables are immutable. Calls on one plan from several host threads take turns
  *     while they enqueue (a per-plan lock); their work on different streams
  *     with distinct workspaces may then run concurrently on the device.
  *   - Compute calls only enqueue work (a hipStream_t, NULL for the default

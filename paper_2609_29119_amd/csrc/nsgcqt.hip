@@ -66,6 +66,7 @@ int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
 struct nsgcqt_plan_s {
     HostPlan h;
     bool device = false;
+    int dev = -1;   // the device that holds the tables (current at creation)
     void* dmem = nullptr;
     int64_t dbytes = 0;
     Tables T{};
@@ -131,6 +132,7 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iRA = add(h.rA.data(), h.rA.size() * sizeof(float));
     const size_t iRSa = add(h.rSa.data(), h.rSa.size() * sizeof(float));
 
+    HIP_TRY(hipGetDevice(&p->dev));
     char* d = nullptr;
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&d), total);
     if (e != hipSuccess) return set_err(NSGCQT_ENOMEM, std::string("hipMalloc of plan tables: ") + hipGetErrorString(e));
@@ -532,10 +534,18 @@ int chain_synthesise(nsgcqt_plan_s* p, const float2* coeffs, float* xo, const fl
     return run_pass_b<true>(p, Y, reinterpret_cast<float2*>(xo), batch, static_cast<long long>(h.L), s);
 }
 
+// in_align / out_align: the alignment in bytes the kernels need of the input
+// and output (8 for complex64 and for signals read or written in pairs, 4 for
+// the sample-wise signal buffers of the sliced calls); the workspace needs 8.
 int check_call(nsgcqt_plan_s* p, const void* in, const void* out, const void* ws, size_t ws_bytes,
-               int64_t need, bool want_sliced) {
+               int64_t need, bool want_sliced, size_t in_align = 8, size_t out_align = 8) {
     if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
     if (!in || !out) return set_err(NSGCQT_EINVAL, "input or output pointer is NULL");
+    auto misaligned = [](const void* q, size_t a) { return (reinterpret_cast<uintptr_t>(q) & (a - 1)) != 0; };
+    if (misaligned(in, in_align) || misaligned(out, out_align) || (ws && misaligned(ws, 8)))
+        return set_err(NSGCQT_EINVAL, "input, output or workspace pointer is not aligned (" +
+                                          std::to_string(in_align) + ", " + std::to_string(out_align) +
+                                          " and 8 bytes)");
     if (p->h.sliced != want_sliced)
         return set_err(NSGCQT_EINVAL, want_sliced ? "plan is not a sliced plan" : "plan is a sliced plan");
     if (static_cast<int64_t>(ws_bytes) < need)
@@ -543,6 +553,11 @@ int check_call(nsgcqt_plan_s* p, const void* in, const void* out, const void* ws
                                               std::to_string(need) + " required");
     if (need > 0 && !ws) return set_err(NSGCQT_EINVAL, "workspace pointer is NULL");
     if (!p->device) return set_err(NSGCQT_EINVAL, "host-only plan has no device tables");
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur));
+    if (cur != p->dev)
+        return set_err(NSGCQT_EINVAL, "plan tables are on device " + std::to_string(p->dev) + ", device " +
+                                          std::to_string(cur) + " is current");
     return NSGCQT_OK;
 }
 
@@ -786,7 +801,7 @@ int64_t nsgcqt_sliced_count(nsgcqt_plan p, int64_t n) {
 
 int nsgcqt_sliced_analyse(nsgcqt_plan p, const float* x, int64_t n, float* coeffs, void* ws, size_t ws_bytes,
                           void* stream) {
-    if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, true)) return r;
+    if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, true, 4, 8)) return r;
     if (n < 1) return set_err(NSGCQT_EINVAL, "signal length must be >= 1");
     std::lock_guard<std::mutex> lock(p->mu);
     const HostPlan& h = p->h;
@@ -804,7 +819,7 @@ int nsgcqt_sliced_analyse(nsgcqt_plan p, const float* x, int64_t n, float* coeff
 
 int nsgcqt_sliced_synthesise(nsgcqt_plan p, const float* coeffs, int64_t n, float* xo, void* ws,
                              size_t ws_bytes, void* stream) {
-    if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, true)) return r;
+    if (int r = check_call(p, coeffs, xo, ws, ws_bytes, p ? p->h.ws_syn : 0, true, 8, 4)) return r;
     if (n < 1) return set_err(NSGCQT_EINVAL, "signal length must be >= 1");
     std::lock_guard<std::mutex> lock(p->mu);
     const HostPlan& h = p->h;

@@ -249,6 +249,22 @@ def test_compute_calls_reject_bad_arguments(lib):
     # a host-only plan with valid arguments has no device tables
     assert lib.nsgcqt_analyse(h, buf, buf, buf, need, None) == nb.EINVAL
     assert b"host-only" in lib.nsgcqt_last_error()
+    # complex64 data, pair-wise signals and the workspace need 8-byte alignment
+    odd = ctypes.c_void_p(20)
+    for args in ((odd, buf, buf), (buf, odd, buf), (buf, buf, odd)):
+        assert lib.nsgcqt_analyse(h, *args, need, None) == nb.EINVAL
+        assert b"aligned" in lib.nsgcqt_last_error()
+    assert lib.nsgcqt_synthesise(h, odd, buf, buf, p.info.ws_synthesise, None) == nb.EINVAL
+    assert b"aligned" in lib.nsgcqt_last_error()
+    # the sliced calls read and write signals sample by sample: 4 bytes do
+    sp = nb.Plan.sliced(22050.0, 110.0, 11025.0, 12, 4096, 2, device=False)
+    sh, sneed = sp._h, max(sp.info.ws_analyse, sp.info.ws_synthesise)
+    assert lib.nsgcqt_sliced_analyse(sh, odd, 100, buf, buf, sneed, None) == nb.EINVAL
+    assert b"host-only" in lib.nsgcqt_last_error()
+    assert lib.nsgcqt_sliced_synthesise(sh, buf, 100, odd, buf, sneed, None) == nb.EINVAL
+    assert b"host-only" in lib.nsgcqt_last_error()
+    assert lib.nsgcqt_sliced_analyse(sh, buf, 100, odd, buf, sneed, None) == nb.EINVAL
+    assert b"aligned" in lib.nsgcqt_last_error()
     assert lib.nsgcqt_band_info(h, p.n_bands, ctypes.byref(nb.BandInfo())) == nb.EINVAL
     assert lib.nsgcqt_plan_weights(h, 9, buf, 1 << 20) == nb.EINVAL
     assert lib.nsgcqt_plan_destroy(None) == nb.OK
