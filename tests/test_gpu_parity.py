@@ -119,6 +119,29 @@ def test_determinism_and_batch_position():
     assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
 
 
+def test_fanned_out_calls_match_single_stream_bitwise():
+    # the training layout at 16 signals fans its band phase out over the
+    # side streams (largest tier first); one signal at a time it runs on one
+    # stream in tier order. Every output bit of every operator agrees.
+    w = workloads.WORKLOADS["train"]
+    b, N = w.batch, w.n_samples
+    pb = nb.Plan(*w.plan_args, batch=b)
+    p1 = nb.Plan(*w.plan_args, batch=1)
+    first = lambda pl: [n for n, _ in pl.stage_info(nb.OP_ANALYSE)][2]
+    assert first(pb) != first(p1)          # the two schedules differ
+    x = workloads.white(91, b, N)
+    y = workloads.coeff_cotangent(92, b, pb.n_coeffs)
+    xg, yg = to_gpu(x), to_gpu(y)
+    outs_b = [to_np(pb.analyse(xg)), to_np(pb.synthesise(yg)),
+              to_np(pb.adjoint(nb.OP_ADJ_ANALYSIS, yg)), to_np(pb.adjoint(nb.OP_ADJ_SYNTHESIS, xg))]
+    for i in (0, 9, b - 1):
+        xi, yi = to_gpu(x[i:i + 1]), to_gpu(y[i:i + 1])
+        outs_1 = [to_np(p1.analyse(xi)), to_np(p1.synthesise(yi)),
+                  to_np(p1.adjoint(nb.OP_ADJ_ANALYSIS, yi)), to_np(p1.adjoint(nb.OP_ADJ_SYNTHESIS, xi))]
+        for k, (ob, o1) in enumerate(zip(outs_b, outs_1)):
+            assert np.array_equal(ob[i].view(np.uint32), o1[0].view(np.uint32)), (i, k)
+
+
 def test_adjoint_identity_fp32():
     w = workloads.WORKLOADS["tiny"]
     p = nb.Plan(*w.plan_args, batch=2)
