@@ -418,3 +418,24 @@ def test_stage_order_follows_the_launch_schedule(lib):
                       "band_analysis_256x8", "band_analysis_64x8"]
     syn = [n for n, _ in train.stage_info(nb.OP_SYNTHESISE)]
     assert syn == [n.replace("analysis", "synthesis") for n in an[2:]] + ["fft_inv_a_overlap_add", "fft_inv_b"]
+
+
+def test_missing_library_fails_loudly():
+    # without the built library there is no fallback: loading it and making a
+    # plan both raise (run in a child so this process keeps its handle)
+    import subprocess
+    import sys
+    code = (
+        "import paper_2609_29119_amd.nsgcqt as nb\n"
+        "nb.LIB_PATH = '/nonexistent/libnsgcqt.so'\n"
+        "for f in (nb.lib, lambda: nb.Plan(22050.0, 110.0, 11025.0, 12, 16384, 1, device=False)):\n"
+        "    try:\n"
+        "        f()\n"
+        "    except RuntimeError as e:\n"
+        "        assert 'missing' in str(e)\n"
+        "    else:\n"
+        "        raise SystemExit('no error')\n"
+        "print('raised')\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120, cwd=root)
+    assert r.returncode == 0 and "raised" in r.stdout, (r.stdout, r.stderr)
