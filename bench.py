@@ -201,7 +201,10 @@ def cpu_baseline(w, x, target_s=12.0, gpu_c=None, gpu_x=None, mode="direct"):
 # HIP kernel (rocprofv3 name) -> stage name reported by nsgcqt_stage_info
 def stage_of_kernel(name):
     import re
-    m = re.search(r"k_(fwd_a|inv_a|pass_b|band_analysis|band_synthesis)<(\d+), (\d+)(?:, (true|false))?>", name)
+    if re.search(r"\bk_ola\b", name):
+        return "sliced_overlap_add"
+    m = re.search(r"k_(fwd_a|inv_a|pass_b|band_analysis|band_synthesis|big_a|big_b)<(\d+), (\d+)(?:, (true|false))?>",
+                  name)
     if not m:
         return None
     k, nt, ept, inv = m.groups()
@@ -211,6 +214,9 @@ def stage_of_kernel(name):
         return "fft_inv_a_overlap_add"
     if k == "pass_b":
         return "fft_inv_b" if inv == "true" else "fft_fwd_b"
+    if k in ("big_a", "big_b"):
+        # one kernel per pass serves both directions
+        return "huge_band_" + ("columns" if k == "big_a" else "rows")
     return f"{k}_{nt}x{ept}"
 
 
@@ -241,6 +247,13 @@ def summarize_profile(trace_dir, fetch_dir, write_dir, workload, command, calib_
             if r["Counter_Name"] != cname:
                 continue
             per.setdefault(r["Kernel_Name"], {}).setdefault(cname, []).append(float(r["Counter_Value"]))
+    if not per:
+        # a kernel trace without counter runs
+        os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+        with open(os.path.join(ROOT, "profiles", f"roundtrip_{workload}.md"), "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        print("\n".join(lines))
+        return
     copy = [v for k, v in per.items() if "copy" in k.lower()]
     calib = None
 

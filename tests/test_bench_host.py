@@ -26,6 +26,9 @@ def test_more_than_one_gpu_is_refused():
     ("void nsg::k_inv_a<512, 8>(...)", "fft_inv_a_overlap_add"),
     ("void nsg::k_band_analysis<256, 8>(...)", "band_analysis_256x8"),
     ("void nsg::k_band_synthesis<1024, 16>(...)", "band_synthesis_1024x16"),
+    ("void nsg::k_big_a<512, 8>(nsg::BigArgs, ...)", "huge_band_columns"),
+    ("void nsg::k_big_b<512, 8>(nsg::BigArgs, ...)", "huge_band_rows"),
+    ("nsg::k_ola(float const*, ...)", "sliced_overlap_add"),
     ("__amd_rocclr_copyBuffer", None),
 ])
 def test_profiler_kernel_names_map_to_stages(name, stage):
