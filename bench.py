@@ -4,7 +4,10 @@ One step = analysis T (packed FFT, routed band inverse FFTs) followed by
 synthesis S (band FFTs, owner overlap-add, packed inverse FFT) over one batch
 of synthetic audio resident in HBM. Default workload: 128 signals of 88,200
 samples at 22.05 kHz, 55 Hz..fs/2 at 36 bins per octave (the throughput
-stress workload). Prints one JSON line.
+stress workload). Prints one JSON line. The default line also carries
+`train_fwdbwd`: the other batched workload, the training front end (16
+signals of 220,500 samples at 44.1 kHz, 40 Hz..fs/2 at 24 bins per octave),
+timed as analysis T followed by its adjoint T^dagger, with its own roofline.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--batch B]
                   [--mode roundtrip|step]
@@ -194,6 +197,9 @@ def cpu_baseline(w, x, target_s=12.0, gpu_c=None, gpu_x=None, mode="direct"):
     if gpu_c is not None and gpu_x is not None:
         out["parity"] = {"signals": k,
                          "coeffs_rel_l2_max": float(oracle.rel_l2(gpu_c[:k], c_ref).max()),
+                         "worst_band_rel_l2": float(oracle.band_rel_l2(gpu_c[:k], c_ref, lay.offsets()).max()),
+                         "worst_band_max_err_over_rms": float(
+                             oracle.band_max_err_over_rms(gpu_c[:k], c_ref, lay.offsets()).max()),
                          "roundtrip_rel_l2_max": float(oracle.rel_l2(gpu_x[:k], x_ref).max())}
     return out
 
@@ -295,6 +301,100 @@ def summarize_profile(trace_dir, fetch_dir, write_dir, workload, command, calib_
     print("\n".join(lines))
 
 
+def time_calls(plan, calls, K, W, use_ev=True):
+    """Times a step made of library calls [(op, fn)] on the current stream:
+    W untimed steps, then (with use_ev) a short pass with every kernel
+    bracketed by HIP events through nsgcqt_set_stage_events, which gives the
+    per-kernel table and names the dominant kernel, then K timed steps with
+    only the dominant kernel bracketed, on the stream it is launched on.
+    Returns the step time (max of the GPU clock and the host wall clock,
+    ms), the allocator peak during the timed steps, the per-kernel table and
+    the dominant kernel's average duration in the timed steps."""
+    import torch
+    infos = [plan.stage_info(op) for op, _ in calls]
+    names = [n for st in infos for n, _ in st]
+    algb = [b for st in infos for _, b in st]
+    nev = [2 * len(st) for st in infos]          # a start and an end event per kernel
+
+    def step(evs=None):
+        for i, (_, f) in enumerate(calls):
+            plan.set_stage_events(None if evs is None else evs[i])
+            f()
+        plan.set_stage_events(None)
+
+    for _ in range(W):
+        step()
+    torch.cuda.synchronize()
+    stages, dom = [], None
+    if use_ev:
+        kc = min(K, 10)
+        per = sum(nev)
+        ev = HipEvents(kc * per)
+        for i in range(kc):
+            base, evs = i * per, []
+            for n in nev:
+                evs.append(ev.ev[base: base + n])
+                base += n
+            step(evs)
+        torch.cuda.synchronize()
+        dur = np.zeros(len(names))
+        for i in range(kc):
+            base = i * per
+            for j in range(len(names)):
+                dur[j] += ev.elapsed_ms(ev.ev[base + 2 * j], ev.ev[base + 2 * j + 1])
+        dur /= kc
+        ev.close()
+        for n_, b_, d_ in zip(names, algb, dur):
+            stages.append({"kernel": n_, "ms": round(float(d_), 5), "alg_bytes": b_,
+                           "GBps": round(b_ / (d_ * 1e-3) / 1e9, 1)})
+        dom = int(np.argmax(dur))
+    evd = HipEvents(2 * K) if dom is not None else None
+
+    def timed_step(i):
+        if evd is None:
+            return step()
+        j, evs = dom, []
+        for n in nev:
+            if 0 <= j < n // 2:
+                evs.append([None] * (2 * j) + [evd.ev[2 * i], evd.ev[2 * i + 1]])
+            else:
+                evs.append(None)
+            j -= n // 2
+        step(evs)
+
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    mem0 = torch.cuda.memory_allocated()
+    t0 = time.perf_counter()
+    t_start.record()
+    for i in range(K):
+        timed_step(i)
+    t_stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    alloc = torch.cuda.max_memory_allocated() - mem0
+    ms = max(t_start.elapsed_time(t_stop), wall * 1e3) / K
+    dom_ms = None
+    if evd is not None:
+        dom_ms = sum(evd.elapsed_ms(evd.ev[2 * i], evd.ev[2 * i + 1]) for i in range(K)) / K
+        evd.close()
+    return {"ms": ms, "alloc": alloc, "names": names, "algb": algb, "stages": stages, "dom": dom,
+            "dom_ms": dom_ms}
+
+
+def roofline(names, algb, dom, dom_ms, workload, traffic_ok):
+    """The dominant kernel's algorithmic bytes over its measured duration
+    against the HBM peak, with its counted traffic from the committed
+    counter summary (None when stale or not for this batch)."""
+    achieved = algb[dom] / (dom_ms * 1e-3) / 1e9
+    return {"bound": "hbm", "kernel": names[dom], "kernel_ms": round(dom_ms, 5),
+            "achieved": round(achieved, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+            "frac": achieved / (HBM_PEAK / 1e9),
+            "traffic": traffic_from_profiles(workload, names[dom]) if traffic_ok else None}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -305,6 +405,8 @@ def main():
     ap.add_argument("--mode", choices=("roundtrip", "step", "fwdbwd"), default="roundtrip")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip the HIP-graph replay timing")
+    ap.add_argument("--no-train", action="store_true",
+                    help="stress round trip only, without the training front end's T + T^dagger leg")
     ap.add_argument("--no-stage-events", action="store_true",
                     help="time the loop without per-kernel events (for profiler runs)")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
@@ -342,82 +444,16 @@ def main():
     xr = torch.empty_like(x)
     ws_a = plan.workspace(nc.OP_ANALYSE)
     ws_s = plan.workspace(nc.OP_SYNTHESISE)
-
-    st_a = plan.stage_info(nc.OP_ANALYSE)
-    st_s = plan.stage_info(nc.OP_SYNTHESISE)
-    names = [n for n, _ in st_a] + [n for n, _ in st_s]
-    algb = [b for _, b in st_a] + [b for _, b in st_s]
-    na, ns = 2 * len(st_a), 2 * len(st_s)      # a start and an end event per kernel
     K, W = args.steps, args.warmup
-    use_ev = not args.no_stage_events
+    calls = [(nc.OP_ANALYSE, lambda: plan.analyse(x, out=c, ws=ws_a)),
+             (nc.OP_SYNTHESISE, lambda: plan.synthesise(c, out=xr, ws=ws_s))]
+    tm = time_calls(plan, calls, K, W, not args.no_stage_events)
+    ms, alloc_steps = tm["ms"], tm["alloc"]
+    names, algb, stages, dom, dom_ms = tm["names"], tm["algb"], tm["stages"], tm["dom"], tm["dom_ms"]
 
-    def step(ev_a=None, ev_s=None):
-        plan.set_stage_events(ev_a)
-        plan.analyse(x, out=c, ws=ws_a)
-        plan.set_stage_events(ev_s)
-        plan.synthesise(c, out=xr, ws=ws_s)
-
-    for _ in range(W):
-        step()
-    torch.cuda.synchronize()
-
-    # Per-kernel table: a short pass with every kernel bracketed (the events
-    # themselves cost a few microseconds each, so this pass is not the timed
-    # one). It also names the dominant kernel.
-    stages, dom = [], None
-    if use_ev:
-        kc = min(K, 10)
-        ev = HipEvents(kc * (na + ns))
-        for i in range(kc):
-            base = i * (na + ns)
-            step(ev.ev[base: base + na], ev.ev[base + na: base + na + ns])
-        torch.cuda.synchronize()
-        plan.set_stage_events(None)
-        dur = np.zeros(len(names))
-        for i in range(kc):
-            base = i * (na + ns)
-            for j in range(len(names)):
-                dur[j] += ev.elapsed_ms(ev.ev[base + 2 * j], ev.ev[base + 2 * j + 1])
-        dur /= kc
-        ev.close()
-        for n_, b_, d_ in zip(names, algb, dur):
-            stages.append({"kernel": n_, "ms": round(float(d_), 5), "alg_bytes": b_,
-                           "GBps": round(b_ / (d_ * 1e-3) / 1e9, 1)})
-        dom = int(np.argmax(dur))
-
-    # Timed region: K steps; only the dominant kernel is bracketed by events,
-    # on the stream it is launched on, for the roofline figure.
-    evd = HipEvents(2 * K) if dom is not None else None
-
-    def timed_step(i):
-        if evd is None:
-            return step()
-        pair = [evd.ev[2 * i], evd.ev[2 * i + 1]]
-        if dom < len(st_a):
-            step([None] * (2 * dom) + pair, None)
-        else:
-            step(None, [None] * (2 * (dom - len(st_a))) + pair)
-
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    torch.cuda.reset_peak_memory_stats()
-    mem0 = torch.cuda.memory_allocated()
-    t0 = time.perf_counter()
-    t_start.record()
-    for i in range(K):
-        timed_step(i)
-    t_stop.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    alloc_steps = torch.cuda.max_memory_allocated() - mem0
-    plan.set_stage_events(None)
-    gpu_ms = t_start.elapsed_time(t_stop)
-    ms = max(gpu_ms, wall * 1e3) / K
-    dom_ms = None
-    if evd is not None:
-        dom_ms = sum(evd.elapsed_ms(evd.ev[2 * i], evd.ev[2 * i + 1]) for i in range(K)) / K
-        evd.close()
+    def step():
+        for _, f in calls:
+            f()
 
     # the same step captured once into a HIP graph and replayed (the paper
     # times round trips under graph replay); the chain records no memsets
@@ -476,15 +512,18 @@ def main():
         "alloc_during_steps_bytes": alloc_steps,
     }
     if dom is not None:
-        achieved = algb[dom] / (dom_ms * 1e-3) / 1e9
-        out["roofline"] = {"bound": "hbm", "kernel": names[dom], "kernel_ms": round(dom_ms, 5),
-                           "achieved": round(achieved, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-                           "frac": achieved / (HBM_PEAK / 1e9),
-                           "traffic": traffic_from_profiles(w.name, names[dom]) if b == w.batch else None}
+        out["roofline"] = roofline(names, algb, dom, dom_ms, w.name, b == w.batch)
         out["stages"] = stages
         counted = counted_step_bytes(w.name, names) if b == w.batch else None
         out["counted_bytes_per_step"] = counted
         out["pct_hbm_peak_counted"] = None if counted is None else 100.0 * counted / (ms * 1e-3) / HBM_PEAK
+    if args.workload == "stress" and not args.batch and not args.no_train:
+        # the other batched workload: the training front end's T + T^dagger
+        wt = workloads.WORKLOADS["train"]
+        pt = make_plan(wt, wt.batch)
+        xt = torch.from_numpy(workloads.signals(wt)).cuda()
+        out["train_fwdbwd"] = fwdbwd_result(wt, pt, xt, K, W, not args.no_stage_events)
+        del pt, xt
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x_np, gpu_c=c.cpu().numpy(), gpu_x=xr_np)
         # the same oracle with pocketfft band transforms: the fairer CPU figure
@@ -544,8 +583,11 @@ def _timed(fn, K, W):
     return (time.perf_counter() - t0) * 1e3 / K
 
 
-def bench_fwdbwd(args, w, plan, x):
-    """Analysis T x, then T^dagger y for a fixed random coefficient cotangent y."""
+def fwdbwd_result(w, plan, x, K, W, use_ev=True):
+    """Analysis T x, then T^dagger y for a fixed random coefficient cotangent
+    y (the training front end's forward and backward): step time, rate,
+    share of the HBM peak on the method's algorithmic bytes, and the roofline
+    of the dominant kernel."""
     import torch
     import workloads
     import paper_2609_29119_amd as nc
@@ -555,21 +597,31 @@ def bench_fwdbwd(args, w, plan, x):
     c = torch.empty((b, C), dtype=torch.complex64, device="cuda")
     g = torch.empty_like(x)
     ws_a, ws_t = plan.workspace(nc.OP_ANALYSE), plan.workspace(nc.OP_ADJ_ANALYSIS)
-
-    def step():
-        plan.analyse(x, out=c, ws=ws_a)
-        plan.adjoint(nc.OP_ADJ_ANALYSIS, y, out=g, ws=ws_t)
-
-    ms = _timed(step, args.steps, args.warmup)
+    calls = [(nc.OP_ANALYSE, lambda: plan.analyse(x, out=c, ws=ws_a)),
+             (nc.OP_ADJ_ANALYSIS, lambda: plan.adjoint(nc.OP_ADJ_ANALYSIS, y, out=g, ws=ws_t))]
+    tm = time_calls(plan, calls, K, W, use_ev)
+    ms = tm["ms"]
     b_alg = (24.0 * N + 16.0 * C) * b      # T: 12N + 8C, T^dagger: 12N + 8C
-    out = {"metric": "CQT analysis forward + adjoint backward audio samples/s and % HBM peak",
-           "value": b * N / (ms * 1e-3), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-           "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-           "config": {"workload": describe(w, b, N) + ", analysis T then adjoint T^dagger",
-                      "batch": b, "n_samples": N, "n_bands": plan.n_bands, "n_coeffs": C},
+    out = {"workload": describe(w, b, N) + ", analysis T then adjoint T^dagger",
+           "ms_per_step": ms, "samples_per_s": b * N / (ms * 1e-3),
            "pct_hbm_peak": 100.0 * b_alg / (ms * 1e-3) / HBM_PEAK, "alg_bytes_per_step": b_alg,
            "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_adjoint_analysis) / b}
+    if tm["dom"] is not None:
+        out["roofline"] = roofline(tm["names"], tm["algb"], tm["dom"], tm["dom_ms"], w.name, b == w.batch)
+        out["stages"] = tm["stages"]
+    return out
+
+
+def bench_fwdbwd(args, w, plan, x):
+    """The training front end's T + T^dagger as the headline of its own line."""
+    b, N = x.shape
+    r = fwdbwd_result(w, plan, x, args.steps, args.warmup, not args.no_stage_events)
+    out = {"metric": "CQT analysis forward + adjoint backward audio samples/s and % HBM peak",
+           "value": r["samples_per_s"], "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": r["ms_per_step"], "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": r["workload"], "batch": b, "n_samples": N, "n_bands": plan.n_bands,
+                      "n_coeffs": plan.n_coeffs}, **{k: v for k, v in r.items() if k != "workload"}}
     print(json.dumps(out), flush=True)
 
 

@@ -363,7 +363,14 @@ int run_fwd_a(nsgcqt_plan_s* p, const float* x, float2* Y, int batch, SliceIn sl
         return NSGCQT_OK;
     };
     if (sl.enabled) {
-        DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a, , true)
+        // the plan keeps sliced column passes at 512 threads or fewer
+        if (p->h.fs4.nt_a == 256) {
+            if (int r = launch(k_fwd_a<256, 8, true>)) return r;
+        } else if (p->h.fs4.nt_a == 512) {
+            if (int r = launch(k_fwd_a<512, 8, true>)) return r;
+        } else {
+            return set_err(NSGCQT_EUNSUPPORTED, "sliced column pass above 512 threads");
+        }
     } else {
         DISPATCH_NT(p->h.fs4.nt_a, k_fwd_a, , false)
     }

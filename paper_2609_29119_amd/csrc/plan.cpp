@@ -695,6 +695,15 @@ int finish_plan(HostPlan& p, std::string& err) {
         };
         pick(f.L1, f.L2, f.tile_a, f.nt_a);
         pick(f.L2, f.L1, f.tile_b, f.nt_b);
+        // the sliced pass A also carries the two samples' clamped positions
+        // and window values per element: at most 512 threads x 8 elements,
+        // so its registers fit without spilling
+        if (sliced) {
+            if (f.L1 > 4096)
+                return fail(err, NSGCQT_EUNSUPPORTED, "slice length too large for the sliced column pass");
+            while (f.tile_a > 0 && (int64_t(1) << f.tile_a) * f.L1 > 4096) --f.tile_a;
+            f.nt_a = std::min(f.nt_a, 512);
+        }
         if ((int64_t(1) << f.tile_a) * f.L1 > 8192 || (int64_t(1) << f.tile_b) * f.L2 > 8192)
             return fail(err, NSGCQT_EUNSUPPORTED, "four-step pass exceeds one workgroup");
         // fewer columns per workgroup until the prime stages' matrix tiles fit

@@ -223,14 +223,22 @@ class Plan:
         return {OP_ANALYSE: i.ws_analyse, OP_SYNTHESISE: i.ws_synthesise,
                 OP_ADJ_ANALYSIS: i.ws_adjoint_analysis, OP_ADJ_SYNTHESIS: i.ws_adjoint_synthesis}[op]
 
-    def workspace(self, op, device=None):
-        """A cached uint8 device buffer big enough for `op`."""
+    def workspace(self, op, device=None, stream=None):
+        """A cached uint8 device buffer big enough for `op`, one per (op,
+        stream): calls on different streams that use the default workspace
+        never share it. It is allocated on that stream (the stream's current
+        one if None), so the caching allocator ties it to the stream that
+        uses it."""
         import torch
         need = max(1, self.workspace_bytes(op))
-        ws = self._ws.get(op)
+        dev = torch.device(device or "cuda")
+        s = torch.cuda.current_stream(dev) if stream is None else stream
+        key = (op, s.cuda_stream)
+        ws = self._ws.get(key)
         if ws is None or ws.numel() < need:
-            ws = torch.empty(need, dtype=torch.uint8, device=device or "cuda")
-            self._ws[op] = ws
+            with torch.cuda.stream(s):
+                ws = torch.empty(need, dtype=torch.uint8, device=dev)
+            self._ws[key] = ws
         return ws
 
     def stage_info(self, op):
@@ -267,7 +275,7 @@ class Plan:
         self._expect(x, torch.float32, (self.batch, self.n_samples))
         out = self._new((self.batch, self.n_coeffs), torch.complex64, x) if out is None else out
         self._expect(out, torch.complex64, (self.batch, self.n_coeffs))
-        ws = self.workspace(OP_ANALYSE, x.device) if ws is None else ws
+        ws = self.workspace(OP_ANALYSE, x.device, stream) if ws is None else ws
         _check(lib().nsgcqt_analyse(self._h, _ptr(x), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
         return out
 
@@ -277,7 +285,7 @@ class Plan:
         self._expect(c, torch.complex64, (self.batch, self.n_coeffs))
         out = self._new((self.batch, self.n_samples), torch.float32, c) if out is None else out
         self._expect(out, torch.float32, (self.batch, self.n_samples))
-        ws = self.workspace(OP_SYNTHESISE, c.device) if ws is None else ws
+        ws = self.workspace(OP_SYNTHESISE, c.device, stream) if ws is None else ws
         _check(lib().nsgcqt_synthesise(self._h, _ptr(c), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
         return out
 
@@ -294,7 +302,7 @@ class Plan:
             raise ValueError("op must be OP_ADJ_ANALYSIS or OP_ADJ_SYNTHESIS")
         out = self._new(shape, dt, inp) if out is None else out
         self._expect(out, dt, shape)
-        ws = self.workspace(op, inp.device) if ws is None else ws
+        ws = self.workspace(op, inp.device, stream) if ws is None else ws
         _check(lib().nsgcqt_adjoint(self._h, int(op), _ptr(inp), _ptr(out), _ptr(ws), ws.numel(),
                                     _stream(stream)))
         return out
@@ -313,7 +321,7 @@ class Plan:
         self._expect(x, torch.float32, (n,))
         out = self._new((J, self.n_coeffs), torch.complex64, x) if out is None else out
         self._expect(out, torch.complex64, (J, self.n_coeffs))
-        ws = self.workspace(OP_ANALYSE, x.device) if ws is None else ws
+        ws = self.workspace(OP_ANALYSE, x.device, stream) if ws is None else ws
         _check(lib().nsgcqt_sliced_analyse(self._h, _ptr(x), n, _ptr(out), _ptr(ws), ws.numel(),
                                            _stream(stream)))
         return out
@@ -325,7 +333,7 @@ class Plan:
         self._expect(c, torch.complex64, (J, self.n_coeffs))
         out = self._new((n,), torch.float32, c) if out is None else out
         self._expect(out, torch.float32, (n,))
-        ws = self.workspace(OP_SYNTHESISE, c.device) if ws is None else ws
+        ws = self.workspace(OP_SYNTHESISE, c.device, stream) if ws is None else ws
         _check(lib().nsgcqt_sliced_synthesise(self._h, _ptr(c), int(n), _ptr(out), _ptr(ws), ws.numel(),
                                               _stream(stream)))
         return out

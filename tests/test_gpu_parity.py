@@ -171,10 +171,26 @@ def test_full_size_workloads_sampled(name):
     cg = to_np(c)
     assert oracle.snr_db(x, xr).min() >= SNR_MIN          # every signal of the batch
     pick = sorted({0, 1, w.batch // 2, w.batch - 1})
-    assert oracle.rel_l2(cg[pick], oracle.analyse(lay, x[pick])).max() <= REL_TOL
+    cref = oracle.analyse(lay, x[pick])
+    assert oracle.rel_l2(cg[pick], cref).max() <= REL_TOL
+    # per band and element-wise, so a localised error cannot hide in the
+    # per-signal norm
+    worst = oracle.band_rel_l2(cg[pick], cref, lay.offsets()).max()
+    elem = oracle.band_max_err_over_rms(cg[pick], cref, lay.offsets()).max()
+    glob = oracle.max_err_over_rms(cg[pick], cref).max()
+    print(f"{name}: worst band relative L2 {worst:.2e}, worst element over its band's rms {elem:.2e}, "
+          f"worst element over the signal's rms {glob:.2e}")
+    # the benchmark spec's bar holds band by band; one element may exceed its band's
+    # relative error by the extreme-value factor of about sqrt(2 ln(2 M)) < 4
+    # for M <= 1,672 bands (coefficient errors are sums of many roundings)
+    assert worst <= REL_TOL
+    assert elem <= 4 * REL_TOL
     y = workloads.coeff_cotangent(w.cot_seed, w.batch, p.n_coeffs)
     ta = to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, to_gpu(y)))
-    assert oracle.rel_l2(ta[pick], oracle.adjoint_analysis(lay, y[pick])).max() <= REL_TOL
+    tref = oracle.adjoint_analysis(lay, y[pick])
+    assert oracle.rel_l2(ta[pick], tref).max() <= REL_TOL
+    print(f"{name}: T-adjoint worst element over the signal's rms "
+          f"{oracle.max_err_over_rms(ta[pick], tref).max():.2e}")
 
 
 def test_sliced_mode_against_oracle():
@@ -193,6 +209,24 @@ def test_sliced_mode_against_oracle():
     xr = to_np(p.sliced_synthesise(c, n))
     assert oracle.snr_db(x, xr) >= SNR_MIN
     np.testing.assert_array_less(oracle.rel_l2(xr, oracle.sliced_synthesise(lay, cref, n)), 1e-5)
+
+
+def test_sliced_largest_column_pass():
+    # slices of 2^19 (L = 512 x 512): the column pass of the sliced path at
+    # its widest configuration (512 threads, 8 columns of 512 per tile);
+    # bands up to 7,600 points (Bluestein), 6 slices in chunks of 2
+    fs, fmin, fmax, bpo, Ns = 44100.0, 100.0, 22050.0, 48, 1 << 19
+    lay = oracle.build_layout(fs, fmin, fmax, bpo, Ns)
+    p = nb.Plan.sliced(fs, fmin, fmax, bpo, Ns, 2)
+    n = 5 * (Ns // 2) - 12345
+    x = workloads.white(7, 1, n)[0]
+    c = p.sliced_analyse(to_gpu(x))
+    cg = to_np(c)
+    cref = oracle.sliced_analyse(lay, x, mode="fft")
+    assert cg.shape == cref.shape == (6, lay.n_coeffs)
+    assert oracle.rel_l2(cg, cref).max() <= REL_TOL
+    xr = to_np(p.sliced_synthesise(c, n))
+    assert oracle.snr_db(x, xr) >= SNR_MIN
 
 
 def test_sliced_table1_layout_against_oracle():
@@ -510,6 +544,33 @@ def test_stage_events_bracket_every_launch_with_side_streams():
         p.set_stage_events(None)
         ev.rt.hipGetLastError()
         ev.close()
+
+
+def test_default_workspace_per_stream():
+    # calls on two streams that rely on the binding's default workspace get
+    # one buffer each, so they do not overwrite each other's intermediates;
+    # results equal the single-stream ones bitwise
+    w = workloads.WORKLOADS["train"]
+    b, N = w.batch, w.n_samples
+    p = nb.Plan(*w.plan_args, batch=b)
+    xs = [to_gpu(workloads.white(90 + i, b, N)) for i in range(2)]
+    ys = [to_gpu(workloads.coeff_cotangent(190 + i, b, p.n_coeffs)) for i in range(2)]
+    ref_c = [to_np(p.analyse(x)) for x in xs]
+    ref_t = [to_np(p.adjoint(nb.OP_ADJ_ANALYSIS, y)) for y in ys]
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    assert p.workspace(nb.OP_ANALYSE, stream=streams[0]).data_ptr() != \
+        p.workspace(nb.OP_ANALYSE, stream=streams[1]).data_ptr()
+    outs_c = [torch.empty((b, p.n_coeffs), dtype=torch.complex64, device="cuda") for _ in range(2)]
+    outs_t = [torch.empty((b, N), dtype=torch.float32, device="cuda") for _ in range(2)]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for i in range(2):      # interleaved enqueues on the two streams
+            p.analyse(xs[i], out=outs_c[i], stream=streams[i])
+            p.adjoint(nb.OP_ADJ_ANALYSIS, ys[i], out=outs_t[i], stream=streams[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        assert np.array_equal(to_np(outs_c[i]).view(np.uint32), ref_c[i].view(np.uint32))
+        assert np.array_equal(to_np(outs_t[i]).view(np.uint32), ref_t[i].view(np.uint32))
 
 
 def test_concurrent_calls_from_threads():

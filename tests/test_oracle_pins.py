@@ -486,3 +486,19 @@ def test_metrics():
     x = np.ones(10)
     assert oracle.snr_db(x, x + 0.1) == pytest.approx(20.0)
     assert oracle.rel_l2(np.array([3.0, 4.0 + 1e-3]), np.array([3.0, 4.0])) == pytest.approx(2e-4)
+
+
+def test_band_metrics():
+    # two bands [0, 2) and [2, 5): errors 3e-3 on (3, 4) and 0 on the second
+    ref = np.array([[3.0, 4.0, 1.0, 2.0, 2.0]], dtype=np.complex128)
+    got = ref.copy()
+    got[0, 1] += 5e-3
+    got[0, 0] += 0.0
+    rb = oracle.band_rel_l2(got, ref, [0, 2])
+    assert rb.shape == (1, 2)
+    assert rb[0, 0] == pytest.approx(1e-3) and rb[0, 1] == 0.0
+    # rms of the row: sqrt((9 + 16 + 1 + 4 + 4) / 5)
+    assert oracle.max_err_over_rms(got, ref)[0] == pytest.approx(5e-3 / np.sqrt(34.0 / 5.0))
+    # per band: 5e-3 over the first band's rms sqrt(25 / 2); 0 in the second
+    bm = oracle.band_max_err_over_rms(got, ref, [0, 2])
+    assert bm[0, 0] == pytest.approx(5e-3 / np.sqrt(12.5)) and bm[0, 1] == 0.0
