@@ -270,6 +270,26 @@ int nsgcqt_plan_weights(nsgcqt_plan plan, int which, float* dst, size_t bytes);
 int nsgcqt_analyse(nsgcqt_plan plan, const float* x, float* coeffs,
                    void* ws, size_t ws_bytes, void* stream);
 
+/* Bytes of the device array that nsgcqt_analyse_noalloc uses as workspace. */
+#define NSGCQT_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* T as nsgcqt_analyse, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same kernels, with the workspace taken from a device
+ * array of NSGCQT_NOALLOC_SCRATCH_BYTES that the library holds on every
+ * device it runs on until the process ends. The call makes no allocation
+ * of any kind. The caller still passes x and coeffs (as for
+ * nsgcqt_analyse); nothing in the array needs to start at zero.
+ * All calls on one device share that device's array, which keeps the last
+ * call's contents: calls that overlap on one device (two streams, or two
+ * host threads with unordered streams) race on it and give wrong results;
+ * order them on one stream.
+ * EWORKSPACE: the plan's analysis workspace (nsgcqt_info.ws_analyse)
+ *             exceeds NSGCQT_NOALLOC_SCRATCH_BYTES.
+ * EINVAL, EDEVICE: as nsgcqt_analyse (EDEVICE also when the array's device
+ *             address cannot be obtained). */
+int nsgcqt_analyse_noalloc(nsgcqt_plan plan, const float* x, float* coeffs, void* stream);
+
 /* S: coeffs [batch][C] c64 -> x_out [batch][N] f32 (eq. 10). */
 int nsgcqt_synthesise(nsgcqt_plan plan, const float* coeffs, float* x_out,
                       void* ws, size_t ws_bytes, void* stream);

@@ -63,6 +63,38 @@ int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
 
 }  // namespace
 
+// Workspace of the allocation-free analysis (nsgcqt_analyse_noalloc). Host
+// code never uses this name as an address: each device's copy is reached
+// through the pointer that hipGetSymbolAddress returns on that device.
+static __device__ __align__(256) char scratch[NSGCQT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, looked up once per
+// device (with that device current) and kept.
+int scratch_address(void** out) {
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return set_err(NSGCQT_EDEVICE, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr)
+            return set_err(NSGCQT_EDEVICE, std::string("hipGetSymbolAddress of the scratch array: ") +
+                                               hipGetErrorString(e));
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return NSGCQT_OK;
+}
+
+}  // namespace
+
 struct nsgcqt_plan_s {
     HostPlan h;
     bool device = false;
@@ -770,6 +802,22 @@ int nsgcqt_plan_weights(nsgcqt_plan p, int which, float* dst, size_t bytes) {
 
 int nsgcqt_analyse(nsgcqt_plan p, const float* x, float* coeffs, void* ws, size_t ws_bytes, void* stream) {
     if (int r = check_call(p, x, coeffs, ws, ws_bytes, p ? p->h.ws_an : 0, false)) return r;
+    std::lock_guard<std::mutex> lock(p->mu);
+    p->ev_next = 0;
+    return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->rA, p->h.batch, SliceIn{0, 0, 0, 0},
+                         static_cast<char*>(ws), static_cast<hipStream_t>(stream));
+}
+
+int nsgcqt_analyse_noalloc(nsgcqt_plan p, const float* x, float* coeffs, void* stream) {
+    if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
+    if (p->h.ws_an > static_cast<int64_t>(NSGCQT_NOALLOC_SCRATCH_BYTES))
+        return set_err(NSGCQT_EWORKSPACE, "the plan's analysis needs " + std::to_string(p->h.ws_an) +
+                                              " bytes of workspace, the allocation-free analysis has " +
+                                              std::to_string(NSGCQT_NOALLOC_SCRATCH_BYTES));
+    if (!p->device) return set_err(NSGCQT_EINVAL, "host-only plan has no device tables");
+    void* ws = nullptr;
+    if (int r = scratch_address(&ws)) return r;
+    if (int r = check_call(p, x, coeffs, ws, NSGCQT_NOALLOC_SCRATCH_BYTES, p->h.ws_an, false)) return r;
     std::lock_guard<std::mutex> lock(p->mu);
     p->ev_next = 0;
     return chain_analyse(p, x, reinterpret_cast<float2*>(coeffs), p->rA, p->h.batch, SliceIn{0, 0, 0, 0},

@@ -29,8 +29,9 @@ EXPORTS = [
     "nsgcqt_sliced_synthesise", "nsgcqt_set_stage_events", "nsgcqt_stage_info",
     "nsgcqt_last_error", "nsgcqt_plan_create_bands", "nsgcqt_plan_create_bands_host",
     "nsgcqt_layout_table1", "nsgcqt_layout_erb", "nsgcqt_sliced_plan_create_bands",
-    "nsgcqt_sliced_plan_create_bands_host",
+    "nsgcqt_sliced_plan_create_bands_host", "nsgcqt_analyse_noalloc",
 ]
+NOALLOC_SCRATCH_BYTES = 64 << 20     # NSGCQT_NOALLOC_SCRATCH_BYTES
 
 
 class NsgcqtError(RuntimeError):
@@ -86,6 +87,7 @@ def lib():
         "nsgcqt_band_info": [P, I, ctypes.POINTER(BandInfo)],
         "nsgcqt_plan_weights": [P, I, V, ctypes.c_size_t],
         "nsgcqt_analyse": [P, V, V, V, ctypes.c_size_t, V],
+        "nsgcqt_analyse_noalloc": [P, V, V, V],
         "nsgcqt_synthesise": [P, V, V, V, ctypes.c_size_t, V],
         "nsgcqt_adjoint": [P, I, V, V, V, ctypes.c_size_t, V],
         "nsgcqt_sliced_count": [P, I64],
@@ -277,6 +279,15 @@ class Plan:
         self._expect(out, torch.complex64, (self.batch, self.n_coeffs))
         ws = self.workspace(OP_ANALYSE, x.device, stream) if ws is None else ws
         _check(lib().nsgcqt_analyse(self._h, _ptr(x), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+        return out
+
+    def analyse_noalloc(self, x, out, stream=None):
+        """As analyse, through nsgcqt_analyse_noalloc: the workspace is the
+        library's device array (no allocation); `out` must be given."""
+        import torch
+        self._expect(x, torch.float32, (self.batch, self.n_samples))
+        self._expect(out, torch.complex64, (self.batch, self.n_coeffs))
+        _check(lib().nsgcqt_analyse_noalloc(self._h, _ptr(x), _ptr(out), _stream(stream)))
         return out
 
     def synthesise(self, c, out=None, ws=None, stream=None):

@@ -249,6 +249,15 @@ def test_compute_calls_reject_bad_arguments(lib):
     # a host-only plan with valid arguments has no device tables
     assert lib.nsgcqt_analyse(h, buf, buf, buf, need, None) == nb.EINVAL
     assert b"host-only" in lib.nsgcqt_last_error()
+    # the allocation-free analysis: the same checks, and plans whose workspace
+    # exceeds its device array are refused before any device call
+    assert lib.nsgcqt_analyse_noalloc(None, buf, buf, None) == nb.EINVAL
+    assert lib.nsgcqt_analyse_noalloc(h, buf, buf, None) == nb.EINVAL
+    assert b"host-only" in lib.nsgcqt_last_error()
+    big = _host_plan(workloads.WORKLOADS["stress"])
+    assert big.info.ws_analyse > nb.NOALLOC_SCRATCH_BYTES
+    assert lib.nsgcqt_analyse_noalloc(big._h, buf, buf, None) == nb.EWORKSPACE
+    assert str(nb.NOALLOC_SCRATCH_BYTES).encode() in lib.nsgcqt_last_error()
     # complex64 data, pair-wise signals and the workspace need 8-byte alignment
     odd = ctypes.c_void_p(20)
     for args in ((odd, buf, buf), (buf, odd, buf), (buf, buf, odd)):
