@@ -258,23 +258,39 @@ int64_t huge_split(int64_t n) {
     return n1;
 }
 
-// Cost of a length-n band transform in its tier, or, above the largest tier,
-// in the four-step huge-band path; infinite when it cannot run. The choice
-// uses the tier's largest interleave (seq_lg for an unbounded batch), so it
-// and hence every result bit do not depend on the batch size.
-double band_fft_cost(int64_t n, int64_t row_bytes) {
+// Where a length-n band transform runs: the tier (-1: the four-step
+// huge-band path) and the largest interleave at which its prime-radix stages'
+// matrix tiles fit that tier's workgroup.
+struct BandFit {
+    int tier;
+    int lg_cap;
+    double cost;
+};
+
+// Cost of a length-n band transform: in the smallest tier that holds it and
+// fits its matrix tiles at some interleave (the largest such interleave up to
+// seq_lg for an unbounded batch), or, above the largest tier, in the
+// four-step huge-band path; infinite when it cannot run. The choice depends on
+// n alone, not on the batch, so every result bit is the same for any batch
+// size and position.
+BandFit band_fft_fit(int64_t n, int64_t row_bytes) {
+    const double inf = std::numeric_limits<double>::infinity();
     std::vector<int> rad;
-    if (!factor_radices(n, rad)) return std::numeric_limits<double>::infinity();
-    const int ti = tier_of(n);
-    if (ti < 0) {
-        if (huge_split(n) < 0) return std::numeric_limits<double>::infinity();
-        return 2.5 * static_cast<double>(n) * static_cast<double>(rad.size());
+    if (!factor_radices(n, rad)) return BandFit{-1, 0, inf};
+    const int t0 = tier_of(n);
+    if (t0 < 0) {
+        if (huge_split(n) < 0) return BandFit{-1, 0, inf};
+        return BandFit{-1, 0, 2.5 * static_cast<double>(n) * static_cast<double>(rad.size())};
     }
-    const Tier& t = kTiers[ti];
-    const int lg = seq_lg(n, t.nt * t.ept, 1 << 30, row_bytes);
-    if (!mfma_fits(rad, n, lg, t.nt)) return std::numeric_limits<double>::infinity();
-    return stage_cost(rad, n, lg);
+    for (int ti = t0; ti < kNumTiers; ++ti) {
+        const Tier& t = kTiers[ti];
+        for (int lg = seq_lg(n, t.nt * t.ept, 1 << 30, row_bytes); lg >= 0; --lg)
+            if (mfma_fits(rad, n, lg, t.nt)) return BandFit{ti, lg, stage_cost(rad, n, lg)};
+    }
+    return BandFit{-1, 0, inf};
 }
+
+double band_fft_cost(int64_t n, int64_t row_bytes) { return band_fft_fit(n, row_bytes).cost; }
 
 // Bluestein length for a band of length M: among the P >= 2M - 1 (up to a
 // quarter longer) whose prime factors are all compile-time radices (2..13),
@@ -738,6 +754,7 @@ int finish_plan(HostPlan& p, std::string& err) {
     p.banddev.clear(); p.chirp.clear(); p.kern.clear();
     const int64_t row_bytes = std::max<int64_t>(p.L + 1, p.C) * 8;
     std::vector<int> work(p.bands.size());
+    std::vector<BandFit> fit(p.bands.size());
     for (size_t l = 0; l < p.bands.size(); ++l) {
         const auto& b = p.bands[l];
         BandDev d{};
@@ -753,8 +770,9 @@ int finish_plan(HostPlan& p, std::string& err) {
         const int64_t M = b.M;
         double c_blu = 0.0;
         const int64_t P = bluestein_length(M, row_bytes, &c_blu);
-        const double c_direct = band_fft_cost(M, row_bytes);
-        if (c_direct <= c_blu || P < 0) {
+        const BandFit fd = band_fft_fit(M, row_bytes);
+        if (fd.cost <= c_blu || P < 0) {
+            fit[l] = fd;
             d.fft = reg.get(M);
             if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no radix plan for a band");
             work[l] = static_cast<int>(M);
@@ -781,6 +799,7 @@ int finish_plan(HostPlan& p, std::string& err) {
             host_dft(bp);
             for (int64_t t = 0; t < P; ++t) push_c(p.kern, bp[t] / static_cast<double>(P));
             work[l] = static_cast<int>(P);
+            fit[l] = band_fft_fit(P, row_bytes);
         }
         p.banddev.push_back(d);
     }
@@ -795,7 +814,7 @@ int finish_plan(HostPlan& p, std::string& err) {
     p.bigs.clear(); p.bigitems.clear(); p.Hn = 0; p.C_big = 0; p.Hn_blu = 0; p.C_big_blu = 0;
     int big_t4 = 0, big_ea = 0, big_eb = 0;
     for (size_t l = 0; l < p.bands.size(); ++l) {
-        const int ti = tier_of(work[l]);
+        const int ti = fit[l].tier;
         if (ti < 0) {
             // four-step through global memory: n = n1 n2, n1 <= n2 <= 4096
             const int64_t n = work[l];
@@ -857,8 +876,8 @@ int finish_plan(HostPlan& p, std::string& err) {
         bk.lds_elems = 0;
         for (int32_t l : bk.bands) {
             const int n = work[l];
-            // 2^lg interleaved signals (seq_lg, as in the cost model)
-            const int lg = seq_lg(n, E, batch, row_bytes);
+            // 2^lg interleaved signals (seq_lg, within the band's matrix-tile cap)
+            const int lg = std::min(seq_lg(n, E, batch, row_bytes), fit[l].lg_cap);
             const int G = 1 << lg;
             bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg));
             for (int s0 = 0; s0 < batch; s0 += G)
