@@ -138,6 +138,40 @@ def counted_step_bytes(workload, kernels):
     return float(sum(t[k] for k in kernels))
 
 
+def stage_elements(label):
+    """{stage: elements one launch produces} of a profiled workload's step
+    (host-only plans; no GPU needed): coefficients for the band kernels,
+    packed-spectrum points for the FFT passes and the overlap-add pass,
+    output samples for the sliced overlap-add. label is a workload name, or
+    long_full / long_sliced for the two round trips of the long workload."""
+    import workloads
+    import paper_2609_29119_amd as nc
+    w = workloads.WORKLOADS[label.split("_")[0]]
+    if label == "long_sliced":
+        plan = nc.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16, device=False)
+        ops, b = (nc.OP_ANALYSE, nc.OP_SYNTHESISE), 16
+    else:
+        b = 1 if w.slice_len else w.batch
+        plan = nc.Plan(*w.plan_args, batch=b, device=False)
+        ops = (nc.OP_ANALYSE, nc.OP_ADJ_ANALYSIS) if w.name == "train" else (nc.OP_ANALYSE, nc.OP_SYNTHESISE)
+    L, C = plan.info.packed_len, plan.n_coeffs
+    out = {}
+    for op in ops:
+        for n, by in plan.stage_info(op):
+            if n.startswith("band_analysis"):
+                e = by / (8.0 * L / C + 8.0)         # (c_b / C) 8 L b + 8 c_b b
+            elif n.startswith("band_synthesis"):
+                e = by / 16.0                        # 16 c_b b
+            elif n == "fft_inv_a_overlap_add":
+                e = by / (8.0 * C / L + 8.0)         # (8 C + 8 L) b
+            elif n == "sliced_overlap_add":
+                e = by / 12.0                        # 6 N b bytes, N / 2 samples per slice
+            else:
+                e = by / 16.0                        # 16 L b
+            out.setdefault(n, e)
+    return out
+
+
 def make_plan(w, batch):
     import paper_2609_29119_amd as nc
     if w.layout == "table1":
@@ -301,6 +335,72 @@ def summarize_profile(trace_dir, fetch_dir, write_dir, workload, command, calib_
     print("\n".join(lines))
 
 
+# SQ counters summarised per kernel (one rocprofv3 --pmc run holds at most 8)
+SQ_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_SMEM", "SQ_INSTS_VMEM_RD",
+               "SQ_INSTS_VMEM_WR", "SQ_WAIT_INST_ANY", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_ACTIVE_INST_VALU",
+               "SQ_ACTIVE_INST_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_ANY", "SQ_INSTS_MFMA", "SQ_ACTIVE_INST_ANY",
+               "SQ_INSTS_VALU_INT32", "SQ_INSTS_VALU_FMA_F32", "SQ_INSTS_VALU_MUL_F32", "SQ_INSTS_VALU_ADD_F32",
+               "SQ_INSTS_VALU_CVT", "SQ_INSTS_BRANCH", "SQ_THREAD_CYCLES_VALU", "SQ_WAIT_INST_LDS")
+
+
+def summarize_counters(sq_dirs, workload, command, elements):
+    """Per-kernel SQ counters (median over the dispatches of each counter
+    run) with per-wave and per-element figures (elements as in
+    stage_elements). Writes profiles/counters_<workload>.json and .md."""
+    import csv
+    import glob
+    import statistics
+    per = {}
+    for d in sq_dirs:
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                st = stage_of_kernel(r["Kernel_Name"])
+                if st and r["Counter_Name"] in SQ_COUNTERS:
+                    per.setdefault(st, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    out = {"workload": workload, "source_hash": kernel_source_hash(), "commands": command, "kernels": {}}
+    lines = [f"# SQ counters per kernel ({workload})", "", "Commands (one per counter run):", "", "```",
+             *command.get("sq", []), "```", "",
+             "Per wave: instructions issued; `wait %` = SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES; `valu %` = "
+             "SQ_ACTIVE_INST_VALU / SQ_WAVE_CYCLES; `lanes` = SQ_THREAD_CYCLES_VALU / SQ_INSTS_VALU "
+             "(active lanes per vector instruction). Per element (a coefficient for the band kernels, a "
+             "packed-spectrum point for the FFT passes and the overlap-add pass): vector "
+             "lane-instructions, split into int32, fp32 (add, mul, fma) and the rest.", "",
+             "| stage | waves | VALU/wave | SALU/wave | LDS/wave | VMEM/wave | MFMA/wave | wait % | valu % | lanes "
+             "| VALU lane-instr / element | int32 | fp32 | other |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for st, c in per.items():
+        m = {k: statistics.median(v) for k, v in c.items()}
+        wv = m.get("SQ_WAVES", 0.0)
+        if not wv:
+            continue
+        k = {"waves": wv}
+        for name in SQ_COUNTERS[1:]:
+            if name in m:
+                k[name] = m[name]
+        out["kernels"][st] = k
+        g = lambda n: m.get(n, float("nan"))   # noqa: E731
+        elems = elements.get(st, float("nan"))
+        valu = g("SQ_INSTS_VALU")
+        i32, fp = g("SQ_INSTS_VALU_INT32"), g("SQ_INSTS_VALU_ADD_F32") + g("SQ_INSTS_VALU_MUL_F32") + g(
+            "SQ_INSTS_VALU_FMA_F32")
+        lanes = g("SQ_THREAD_CYCLES_VALU") / valu if valu else float("nan")
+        k["valu_lane_instr_per_element"] = 64.0 * valu / elems
+        k["active_lanes_per_valu_instr"] = lanes
+        lines.append(
+            f"| {st} | {wv:.0f} | {valu / wv:.0f} | {g('SQ_INSTS_SALU') / wv:.0f} | {g('SQ_INSTS_LDS') / wv:.0f} | "
+            f"{(g('SQ_INSTS_VMEM_RD') + g('SQ_INSTS_VMEM_WR')) / wv:.0f} | {g('SQ_INSTS_MFMA') / wv:.1f} | "
+            f"{100 * g('SQ_WAIT_INST_ANY') / g('SQ_WAVE_CYCLES'):.0f} | "
+            f"{100 * g('SQ_ACTIVE_INST_VALU') / g('SQ_WAVE_CYCLES'):.0f} | {lanes:.0f} | "
+            f"{64 * valu / elems:.0f} | {64 * i32 / elems:.0f} | {64 * fp / elems:.0f} | "
+            f"{64 * (valu - i32 - fp) / elems:.0f} |")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"counters_{workload}.json"), "w") as fh:
+        json.dump(out, fh, indent=1)
+    with open(os.path.join(ROOT, "profiles", f"counters_{workload}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def time_calls(plan, calls, K, W, use_ev=True):
     """Times a step made of library calls [(op, fn)] on the current stream:
     W untimed steps, then (with use_ev) a short pass with every kernel
@@ -414,7 +514,15 @@ def main():
     ap.add_argument("--summarize-profile", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="summarise rocprofv3 outputs into profiles/ and exit")
     ap.add_argument("--commands", default="{}", help="JSON of the profiler commands (for the summary)")
+    ap.add_argument("--long-part", choices=("both", "full", "sliced"), default="both",
+                    help="long workload: which round trip(s) to time")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="SQ_DIR",
+                    help="summarise rocprofv3 SQ counter runs into profiles/ and exit")
     args = ap.parse_args()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.workload, json.loads(args.commands),
+                           stage_elements(args.workload))
+        return
     if args.summarize_profile:
         summarize_profile(*args.summarize_profile, args.workload, json.loads(args.commands),
                           args.copy_calib_mb * 1024 * 1024)
@@ -627,8 +735,11 @@ def bench_fwdbwd(args, w, plan, x):
 
 def bench_long(args, w):
     """The 60 s signal: full-length round trip and sliced round trip, each
-    with its plan's workspace and the device-memory high-water mark of the
-    call beyond its inputs and outputs."""
+    with its per-kernel table and roofline (the sliced calls' kernels are
+    those of one chunk of slices, timed on the first chunk), its plan's
+    workspace and the device-memory high-water mark of the calls beyond
+    their inputs and outputs. --long-part picks one of the two (profiler
+    runs take each alone, so their counters are attributed to it)."""
     import torch
     import workloads
     import paper_2609_29119_amd as nc
@@ -636,57 +747,66 @@ def bench_long(args, w):
     x_np = workloads.signals(w)
     x = torch.from_numpy(x_np).cuda()
     N = w.n_samples
+    K, W = args.steps, args.warmup
+    use_ev = not args.no_stage_events
     res = {}
-    # full length: one plan over all N samples
-    plan = nc.Plan(*w.plan_args, batch=1)
-    c = torch.empty((1, plan.n_coeffs), dtype=torch.complex64, device="cuda")
-    xr = torch.empty_like(x)
-    ws_a, ws_s = plan.workspace(nc.OP_ANALYSE), plan.workspace(nc.OP_SYNTHESISE)
 
-    def full():
-        plan.analyse(x, out=c, ws=ws_a)
-        plan.synthesise(c, out=xr, ws=ws_s)
+    def timing(plan, calls, label, b_alg):
+        tm = time_calls(plan, calls, K, W, use_ev)
+        r = {"ms_per_step": tm["ms"], "samples_per_s": N / (tm["ms"] * 1e-3),
+             "alg_bytes_per_step": b_alg, "pct_hbm_peak": 100.0 * b_alg / (tm["ms"] * 1e-3) / HBM_PEAK,
+             "alloc_peak_during_calls_bytes": int(tm["alloc"])}
+        if tm["dom"] is not None:
+            r["roofline"] = roofline(tm["names"], tm["algb"], tm["dom"], tm["dom_ms"], label, True)
+            r["stages"] = tm["stages"]
+        return r
 
-    ms = _timed(full, args.steps, args.warmup)
-    e = (x_np[0].astype(np.float64) - xr.cpu().numpy()[0])
-    snr = 10 * np.log10(np.sum(x_np.astype(np.float64) ** 2) / np.sum(e ** 2))
-    res["full"] = {"ms_per_step": ms, "samples_per_s": N / (ms * 1e-3), "snr_db": float(snr),
-                   "n_bands": plan.n_bands, "n_coeffs": plan.n_coeffs,
-                   "workspace_bytes": max(plan.info.ws_analyse, plan.info.ws_synthesise),
-                   "table_bytes": plan.info.table_bytes,
-                   "pct_hbm_peak": 100.0 * (24.0 * N + 16.0 * plan.n_coeffs) / (ms * 1e-3) / HBM_PEAK}
-    del plan, c, xr, ws_a, ws_s
-    torch.cuda.synchronize()
-    torch.cuda.empty_cache()
-    # sliced: slices of slice_len, 50 % overlap, 16 slices per chunk
-    sp = nc.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16)
-    x1 = x[0].contiguous()
-    J = sp.slice_count(N)
-    cs = torch.empty((J, sp.n_coeffs), dtype=torch.complex64, device="cuda")
-    xs = torch.empty_like(x1)
-    wa, wsn = sp.workspace(nc.OP_ANALYSE), sp.workspace(nc.OP_SYNTHESISE)
-
-    def sliced():
-        sp.sliced_analyse(x1, out=cs, ws=wa)
-        sp.sliced_synthesise(cs, N, out=xs, ws=wsn)
-
-    torch.cuda.synchronize()
-    base = torch.cuda.memory_allocated()
-    torch.cuda.reset_peak_memory_stats()
-    ms = _timed(sliced, args.steps, args.warmup)
-    peak = torch.cuda.max_memory_allocated() - base
-    e = x_np[0].astype(np.float64) - xs.cpu().numpy()
-    snr = 10 * np.log10(np.sum(x_np.astype(np.float64) ** 2) / np.sum(e ** 2))
-    res["sliced"] = {"ms_per_step": ms, "samples_per_s": N / (ms * 1e-3), "snr_db": float(snr),
-                     "slices": J, "slice_len": w.slice_len, "coeffs_per_slice": sp.n_coeffs,
-                     "workspace_bytes": max(sp.info.ws_analyse, sp.info.ws_synthesise),
-                     "table_bytes": sp.info.table_bytes, "alloc_peak_during_calls_bytes": int(peak)}
+    if args.long_part in ("both", "full"):
+        # full length: one plan over all N samples
+        plan = nc.Plan(*w.plan_args, batch=1)
+        c = torch.empty((1, plan.n_coeffs), dtype=torch.complex64, device="cuda")
+        xr = torch.empty_like(x)
+        ws_a, ws_s = plan.workspace(nc.OP_ANALYSE), plan.workspace(nc.OP_SYNTHESISE)
+        calls = [(nc.OP_ANALYSE, lambda: plan.analyse(x, out=c, ws=ws_a)),
+                 (nc.OP_SYNTHESISE, lambda: plan.synthesise(c, out=xr, ws=ws_s))]
+        r = timing(plan, calls, "long_full", 24.0 * N + 16.0 * plan.n_coeffs)
+        e = (x_np[0].astype(np.float64) - xr.cpu().numpy()[0])
+        r.update({"snr_db": float(10 * np.log10(np.sum(x_np.astype(np.float64) ** 2) / np.sum(e ** 2))),
+                  "n_bands": plan.n_bands, "n_coeffs": plan.n_coeffs,
+                  "workspace_bytes": max(plan.info.ws_analyse, plan.info.ws_synthesise),
+                  "table_bytes": plan.info.table_bytes})
+        res["full"] = r
+        del plan, c, xr, ws_a, ws_s, calls
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    if args.long_part in ("both", "sliced"):
+        # sliced: slices of slice_len, 50 % overlap, 16 slices per chunk
+        sp = nc.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16)
+        x1 = x[0].contiguous()
+        J = sp.slice_count(N)
+        cs = torch.empty((J, sp.n_coeffs), dtype=torch.complex64, device="cuda")
+        xs = torch.empty_like(x1)
+        wa, wsn = sp.workspace(nc.OP_ANALYSE), sp.workspace(nc.OP_SYNTHESISE)
+        calls = [(nc.OP_ANALYSE, lambda: sp.sliced_analyse(x1, out=cs, ws=wa)),
+                 (nc.OP_SYNTHESISE, lambda: sp.sliced_synthesise(cs, N, out=xs, ws=wsn))]
+        # per slice the method's round-trip bytes at slice length
+        r = timing(sp, calls, "long_sliced", J * (24.0 * w.slice_len + 16.0 * sp.n_coeffs))
+        e = x_np[0].astype(np.float64) - xs.cpu().numpy()
+        r.update({"snr_db": float(10 * np.log10(np.sum(x_np.astype(np.float64) ** 2) / np.sum(e ** 2))),
+                  "slices": J, "slice_len": w.slice_len, "slices_per_chunk": 16,
+                  "coeffs_per_slice": sp.n_coeffs,
+                  "workspace_bytes": max(sp.info.ws_analyse, sp.info.ws_synthesise),
+                  "table_bytes": sp.info.table_bytes})
+        res["sliced"] = r
+    head = res.get("full") or res["sliced"]
     out = {"metric": "CQT analysis+synthesis round-trip audio samples/s (full-length and sliced); peak workspace",
-           "value": res["full"]["samples_per_s"], "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": res["full"]["ms_per_step"], "higher_is_better": True,
+           "value": head["samples_per_s"], "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": head["ms_per_step"], "higher_is_better": True,
            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
            "config": {"workload": f"{w.name}: 1 x {N} samples @ {w.fs:g} Hz, {w.fmin:g} Hz..fs/2, "
-                                  f"{w.bins_per_octave} bins/oct, full-length and sliced round trips"},
+                                  f"{w.bins_per_octave} bins/oct, "
+                                  + {"both": "full-length and sliced round trips", "full": "full-length round trip",
+                                     "sliced": "sliced round trip"}[args.long_part]},
            **res}
     print(json.dumps(out), flush=True)
 

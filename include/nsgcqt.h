@@ -325,11 +325,16 @@ int nsgcqt_sliced_synthesise(nsgcqt_plan plan, const float* coeffs, int64_t n, f
  * is plan state: do not combine it with concurrent calls on the same plan. */
 int nsgcqt_set_stage_events(nsgcqt_plan plan, void* const* events, int n_events);
 
-/* Kernels one call of `op` enqueues (non-sliced plans), in enqueue order:
- * returns their count (>= 0) or a negative status. For i in range, writes the kernel's
- * name and the algorithmic bytes one launch must move (inputs read once,
- * outputs written once; persistent tables excluded). name/alg_bytes may be
- * NULL. */
+/* Kernels one call of `op` enqueues, in enqueue order: returns their count
+ * (>= 0) or a negative status. For i in range, writes the kernel's name and
+ * the algorithmic bytes one launch must move (inputs read once, outputs
+ * written once; persistent tables excluded). name/alg_bytes may be NULL.
+ * For a sliced plan (Sec. 4 slicing) the list is that of one chunk of
+ * slices_per_chunk slices, which a sliced call repeats per chunk (the last
+ * chunk may hold fewer slices): NSGCQT_OP_ANALYSE gives the analysis chain,
+ * NSGCQT_OP_SYNTHESISE the synthesis chain followed by the overlap-add of the
+ * chunk's slices; other ops are EINVAL. Stage events then bracket the
+ * kernels of the first chunk. */
 int nsgcqt_stage_info(nsgcqt_plan plan, int op, int i, char* name, size_t name_cap,
                       double* alg_bytes);
 

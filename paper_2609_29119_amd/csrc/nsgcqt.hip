@@ -915,9 +915,13 @@ int nsgcqt_set_stage_events(nsgcqt_plan p, void* const* events, int n_events) {
 
 int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, double* alg_bytes) {
     if (!p) return set_err(NSGCQT_EINVAL, "plan is NULL");
-    if (p->h.sliced) return set_err(NSGCQT_EUNSUPPORTED, "stage info is reported for non-sliced plans");
     if (op < 0 || op > 3) return set_err(NSGCQT_EINVAL, "unknown op");
     const HostPlan& h = p->h;
+    // a sliced plan lists the kernels of one chunk of h.batch (= slices per
+    // chunk) slices: the analysis chain, or the synthesis chain and the
+    // overlap-add of the chunk's slices
+    if (h.sliced && op != NSGCQT_OP_ANALYSE && op != NSGCQT_OP_SYNTHESISE)
+        return set_err(NSGCQT_EINVAL, "a sliced plan runs analysis and synthesis only");
     const double b = h.batch, L = static_cast<double>(h.L), C = static_cast<double>(h.C);
     struct St { std::string name; double bytes; };
     std::vector<St> st;
@@ -956,6 +960,9 @@ int nsgcqt_stage_info(nsgcqt_plan p, int op, int i, char* name, size_t cap, doub
     if (!an) {
         st.push_back({"fft_inv_a_overlap_add", (8.0 * C + 8.0 * L) * b});
         st.push_back({"fft_inv_b", 16.0 * L * b});
+        // per slice: read its N synthesised samples, write the H = N / 2
+        // output samples it completes
+        if (h.sliced) st.push_back({"sliced_overlap_add", 6.0 * static_cast<double>(h.N) * b});
     }
     if (i >= 0 && i < static_cast<int>(st.size())) {
         if (name && cap) {

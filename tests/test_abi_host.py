@@ -429,6 +429,20 @@ def test_stage_order_follows_the_launch_schedule(lib):
     assert syn == [n.replace("analysis", "synthesis") for n in an[2:]] + ["fft_inv_a_overlap_add", "fft_inv_b"]
 
 
+def test_sliced_stage_info_lists_one_chunk(lib):
+    # a sliced plan reports the kernels of one chunk of slices: the analysis
+    # chain, and the synthesis chain followed by the overlap-add
+    w = workloads.WORKLOADS["long"]
+    sp = nb.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16, device=False)
+    plain = nb.Plan(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16, device=False)
+    an, syn = sp.stage_info(nb.OP_ANALYSE), sp.stage_info(nb.OP_SYNTHESISE)
+    assert an == plain.stage_info(nb.OP_ANALYSE)
+    assert syn[:-1] == plain.stage_info(nb.OP_SYNTHESISE)
+    assert syn[-1] == ("sliced_overlap_add", 6.0 * w.slice_len * 16)
+    for op in (nb.OP_ADJ_ANALYSIS, nb.OP_ADJ_SYNTHESIS):
+        assert lib.nsgcqt_stage_info(sp._h, op, -1, None, 0, None) == nb.EINVAL
+
+
 def test_missing_library_fails_loudly():
     # without the built library there is no fallback: loading it and making a
     # plan both raise (run in a child so this process keeps its handle)

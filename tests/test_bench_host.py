@@ -87,3 +87,25 @@ def test_source_hash_ignores_comments_and_layout():
     # code and string literals still count
     assert bench.strip_c_comments(a) != bench.strip_c_comments(a.replace("+ 1", "+ 2"))
     assert bench.strip_c_comments(a) != bench.strip_c_comments(a.replace('"a // b"', '"a // c"'))
+
+
+@pytest.mark.parametrize("label", ["stress", "train", "long_full", "long_sliced"])
+def test_stage_elements_count_coefficients_and_points(label):
+    # the counter summary's per-element figures: the band kernels of one
+    # direction produce every coefficient of the step once, the FFT passes
+    # transform L points per signal
+    import workloads
+    from paper_2609_29119_amd import nsgcqt as nb
+    e = bench.stage_elements(label)
+    w = workloads.WORKLOADS[label.split("_")[0]]
+    if label == "long_sliced":
+        p, b = nb.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 16, device=False), 16
+    else:
+        b = 1 if w.slice_len else w.batch
+        p = nb.Plan(*w.plan_args, batch=b, device=False)
+    an = sum(v for k, v in e.items() if k.startswith("band_analysis"))
+    if label != "long_full":     # the full-length long plan also has huge bands
+        assert an == pytest.approx(p.n_coeffs * b, rel=1e-9)
+    assert e["fft_fwd_a"] == pytest.approx(p.info.packed_len * b, rel=1e-12)
+    assert e["fft_inv_a_overlap_add" if label != "train" else "fft_fwd_b"] == pytest.approx(
+        p.info.packed_len * b, rel=1e-9)
