@@ -211,6 +211,41 @@ def test_sliced_mode_against_oracle():
     np.testing.assert_array_less(oracle.rel_l2(xr, oracle.sliced_synthesise(lay, cref, n)), 1e-5)
 
 
+def test_sliced_stage_events_bracket_the_first_chunk():
+    # a sliced call repeats one chunk's kernels (nsgcqt_stage_info on the
+    # sliced plan) per chunk of slices; stage events bracket those of the
+    # first chunk, each pair timing a positive interval, and leave the
+    # results bitwise unchanged
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import HipEvents
+    w = workloads.WORKLOADS["long"]
+    p = nb.Plan.sliced(w.fs, w.fmin, w.fmax, w.bins_per_octave, w.slice_len, 4)
+    n = 600001                      # 11 slices: chunks of 4, 4 and 3
+    x = to_gpu(workloads.white(w.seed, 1, n)[0])
+    ce = to_np(p.sliced_analyse(x))
+    xe = to_np(p.sliced_synthesise(to_gpu(ce), n))
+    sa, ss = p.stage_info(nb.OP_ANALYSE), p.stage_info(nb.OP_SYNTHESISE)
+    assert ss[-1][0] == "sliced_overlap_add"
+    ev = HipEvents(2 * len(sa) + 2 * len(ss))
+    try:
+        ea, es = ev.ev[:2 * len(sa)], ev.ev[2 * len(sa):]
+        p.set_stage_events(ea)
+        c = p.sliced_analyse(x)
+        p.set_stage_events(es)
+        xr = p.sliced_synthesise(c, n)
+        p.set_stage_events(None)
+        assert np.array_equal(to_np(c).view(np.uint32), ce.view(np.uint32))
+        assert np.array_equal(to_np(xr).view(np.uint32), xe.view(np.uint32))
+        for evs, st in ((ea, sa), (es, ss)):
+            for i in range(len(st)):
+                assert ev.elapsed_ms(evs[2 * i], evs[2 * i + 1]) > 0.0, st[i][0]
+    finally:
+        p.set_stage_events(None)
+        ev.close()
+
+
 def test_sliced_largest_column_pass():
     # slices of 2^19 (L = 512 x 512): the column pass of the sliced path at
     # its widest configuration (512 threads, 8 columns of 512 per tile);
