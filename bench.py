@@ -579,26 +579,7 @@ def main():
 
     # the same step captured once into a HIP graph and replayed (the paper
     # times round trips under graph replay); the chain records no memsets
-    graph_ms = None
-    if not args.no_graph:
-        cur = torch.cuda.current_stream()
-        side = torch.cuda.Stream()
-        side.wait_stream(cur)
-        with torch.cuda.stream(side):
-            step()
-        cur.wait_stream(side)
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            step()
-        for _ in range(W):
-            g.replay()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(K):
-            g.replay()
-        torch.cuda.synchronize()
-        graph_ms = (time.perf_counter() - t0) * 1e3 / K
-        del g
+    graph_ms = None if args.no_graph else graph_replay_ms(step, K, W)
 
     calib_copies(args.copy_calib_mb)
 
@@ -638,7 +619,7 @@ def main():
         wt = workloads.WORKLOADS["train"]
         pt = make_plan(wt, wt.batch)
         xt = torch.from_numpy(workloads.signals(wt)).cuda()
-        out["train_fwdbwd"] = fwdbwd_result(wt, pt, xt, K, W, not args.no_stage_events)
+        out["train_fwdbwd"] = fwdbwd_result(wt, pt, xt, K, W, not args.no_stage_events, not args.no_graph)
         del pt, xt
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, x_np, gpu_c=c.cpu().numpy(), gpu_x=xr_np)
@@ -699,11 +680,36 @@ def _timed(fn, K, W):
     return (time.perf_counter() - t0) * 1e3 / K
 
 
-def fwdbwd_result(w, plan, x, K, W, use_ev=True):
+def graph_replay_ms(step, K, W):
+    """Mean time per replay of `step` captured once into a HIP graph (ms),
+    after one eager run on a side stream and W untimed replays."""
+    import torch
+    cur = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(cur)
+    with torch.cuda.stream(side):
+        step()
+    cur.wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for _ in range(W):
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        g.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / K
+    del g
+    return ms
+
+
+def fwdbwd_result(w, plan, x, K, W, use_ev=True, graph=True):
     """Analysis T x, then T^dagger y for a fixed random coefficient cotangent
     y (the training front end's forward and backward): step time, rate,
-    share of the HBM peak on the method's algorithmic bytes, and the roofline
-    of the dominant kernel."""
+    share of the HBM peak on the method's algorithmic bytes, the roofline
+    of the dominant kernel, and the step's time under HIP-graph replay."""
     import torch
     import workloads
     import paper_2609_29119_amd as nc
@@ -722,6 +728,7 @@ def fwdbwd_result(w, plan, x, K, W, use_ev=True):
            "ms_per_step": ms, "samples_per_s": b * N / (ms * 1e-3),
            "pct_hbm_peak": 100.0 * b_alg / (ms * 1e-3) / HBM_PEAK, "alg_bytes_per_step": b_alg,
            "workspace_bytes_per_signal": max(plan.info.ws_analyse, plan.info.ws_adjoint_analysis) / b}
+    out["graph_replay_ms_per_step"] = graph_replay_ms(lambda: [f() for _, f in calls], K, W) if graph else None
     if tm["dom"] is not None:
         out["roofline"] = roofline(tm["names"], tm["algb"], tm["dom"], tm["dom_ms"], w.name, b == w.batch)
         out["stages"] = tm["stages"]
@@ -731,7 +738,7 @@ def fwdbwd_result(w, plan, x, K, W, use_ev=True):
 def bench_fwdbwd(args, w, plan, x):
     """The training front end's T + T^dagger as the headline of its own line."""
     b, N = x.shape
-    r = fwdbwd_result(w, plan, x, args.steps, args.warmup, not args.no_stage_events)
+    r = fwdbwd_result(w, plan, x, args.steps, args.warmup, not args.no_stage_events, not args.no_graph)
     calib_copies(args.copy_calib_mb)
     out = {"metric": "CQT analysis forward + adjoint backward audio samples/s and % HBM peak",
            "value": r["samples_per_s"], "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
