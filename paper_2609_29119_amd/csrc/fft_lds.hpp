@@ -53,6 +53,8 @@ struct Div {
     int d;
 };
 __device__ __forceinline__ Div mkdiv(int d) { return Div{1.0f / static_cast<float>(d), d}; }
+// The same from a reciprocal the plan rounded once to fp32 (FftDesc).
+__device__ __forceinline__ Div mkdiv(int d, float r) { return Div{r, d}; }
 __device__ __forceinline__ int qdiv(int x, Div v, int& rem) {
     int q = static_cast<int>(static_cast<float>(x) * v.r);
     int r = x - __mul24(q, v.d);
@@ -213,7 +215,7 @@ template <> struct Dft<16> { __device__ __forceinline__ static void run(float2* 
 // the length-R DFT, and after a barrier writes out[(jj - k) R + k + r Ns].
 // The twiddles omega_{Ns R}^{r k} come precomputed per stage (tws).
 template <int R, int NT, int EPT>
-__device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb, int Ns,
+__device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb, int Ns, float rns,
                                             const float2* __restrict__ tws) {
     constexpr int BPT = (EPT + R - 1) / R;
     const int tid = stage_tid();
@@ -221,7 +223,7 @@ __device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb,
     const int total = m << lgnb;
     const int nbm = (1 << lgnb) - 1;
     const int mS = __mul24(m, S), NsS = __mul24(Ns, S);
-    const Div dns = mkdiv(Ns);
+    const Div dns = mkdiv(Ns, rns);
     float2 v[BPT][R];
     int ob[BPT];
 #pragma unroll
@@ -267,15 +269,15 @@ __device__ __forceinline__ void stage_fixed(float2* buf, int n, int S, int lgnb,
 // and replaced in place by s_r = y_r + y_{R-r} (at r) and d_r = y_r - y_{R-r}
 // (at R - r). Input 0 carries no twiddle.
 template <int NT>
-__device__ __forceinline__ void prime_fold(float2* buf, int n, int S, int lgnb, int Ns, int R,
-                                           const float2* __restrict__ tws) {
+__device__ __forceinline__ void prime_fold(float2* buf, int n, int S, int lgnb, int Ns, int R, float rns,
+                                           float rh, const float2* __restrict__ tws) {
     const int tid = stage_tid();
     const int m = n / R;
     const int h = (R - 1) >> 1;
     const int nbm = (1 << lgnb) - 1;
     const int mS = __mul24(m, S);
     const int totb = m << lgnb;
-    const Div dns = mkdiv(Ns), dh = mkdiv(h);
+    const Div dns = mkdiv(Ns, rns), dh = mkdiv(h, rh);
     const int total = __mul24(totb, h);
     // four pairs at a time, all twiddle reads issued first
     constexpr int U = 4;
@@ -331,11 +333,12 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // them until every wave has read its inputs; the caller guarantees
 // mfma_tiles(totb, R) <= kMfmaTilesPerWave * NT / 64.
 template <int NT>
-__device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int lgnb, int Ns, int R,
-                                                 const float2* __restrict__ tws, const float* __restrict__ amat) {
+__device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int lgnb, int Ns, int R, float rns,
+                                                 float rh, const float2* __restrict__ tws,
+                                                 const float* __restrict__ amat) {
     constexpr int NW = NT / 64;
     constexpr int TPW = kMfmaTilesPerWave;
-    prime_fold<NT>(buf, n, S, lgnb, Ns, R, tws);
+    prime_fold<NT>(buf, n, S, lgnb, Ns, R, rns, rh, tws);
     __syncthreads();
     const int tid = stage_tid();
     const int lane = tid & 63, wave = tid >> 6;
@@ -346,6 +349,9 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
     const int totb = m << lgnb;
     const int Qb = (h + 16) >> 4, Kb = (h + 3) >> 2;
     const int ntiles = ((totb + 7) >> 3) * Qb;
+    // tile = cb Qb + qb with tile < 2^12 and Qb <= 17: (tile + 1/2) / Qb is at
+    // least 1/34 from an integer, far beyond the reciprocal's error
+    const float rqb = __builtin_amdgcn_rcpf(static_cast<float>(Qb));
     const int kk = lane >> 4, part = lane & 1;
     float* fb = reinterpret_cast<float*>(buf);
     f32x4 dc[TPW], ds[TPW];
@@ -357,7 +363,7 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
         ds[i] = f32x4{0.f, 0.f, 0.f, 0.f};
         y0[i] = 0.f;
         if (tile < ntiles) {
-            const int qb = tile % Qb, cb = tile / Qb;
+            const int cb = static_cast<int>((static_cast<float>(tile) + 0.5f) * rqb), qb = tile - cb * Qb;
             const int c = min((cb << 3) + ((lane & 15) >> 1), totb - 1);
             const int a0 = __mul24(c >> lgnb, S) + (c & nbm);
             // s_r.part at input r, d_r.(1 - part) at input R - r (r = 4 kb + kk + 1;
@@ -399,12 +405,12 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
         }
     }
     __syncthreads();
-    const Div dns = mkdiv(Ns);
+    const Div dns = mkdiv(Ns, rns);
 #pragma unroll
     for (int i = 0; i < TPW; ++i) {
         const int tile = wave + i * NW;
         if (tile < ntiles) {
-            const int qb = tile % Qb, cb = tile / Qb;
+            const int cb = static_cast<int>((static_cast<float>(tile) + 0.5f) * rqb), qb = tile - cb * Qb;
             const int c = (cb << 3) + ((lane & 15) >> 1);
             if (c < totb) {
                 const int t = c & nbm, jj = c >> lgnb;
@@ -443,25 +449,27 @@ __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftD
     int Ns = 1;
     for (int s = 0; s < ns; ++s) {
         const int R = d->radix[s];
+        const float rns = d->rcp_ns[s];
         const float2* tw = stw + d->stoff[s];
         switch (R) {
-            case 2: stage_fixed<2, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 3: stage_fixed<3, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 4: stage_fixed<4, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 5: stage_fixed<5, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 6: stage_fixed<6, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 7: stage_fixed<7, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 8: stage_fixed<8, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 9: stage_fixed<9, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 10: stage_fixed<10, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 11: stage_fixed<11, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 12: stage_fixed<12, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 13: stage_fixed<13, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 14: stage_fixed<14, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 15: stage_fixed<15, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
-            case 16: stage_fixed<16, NT, EPT>(buf, n, S, lgnb, Ns, tw); break;
+            case 2: stage_fixed<2, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 3: stage_fixed<3, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 4: stage_fixed<4, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 5: stage_fixed<5, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 6: stage_fixed<6, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 7: stage_fixed<7, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 8: stage_fixed<8, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 9: stage_fixed<9, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 10: stage_fixed<10, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 11: stage_fixed<11, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 12: stage_fixed<12, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 13: stage_fixed<13, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 14: stage_fixed<14, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 15: stage_fixed<15, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
+            case 16: stage_fixed<16, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
             default:
-                stage_prime_mfma<NT>(buf, n, S, lgnb, Ns, R, tw, reinterpret_cast<const float*>(pool + d->mat[s]));
+                stage_prime_mfma<NT>(buf, n, S, lgnb, Ns, R, rns, d->rcp_h[s], tw,
+                                     reinterpret_cast<const float*>(pool + d->mat[s]));
                 break;
         }
         Ns *= R;

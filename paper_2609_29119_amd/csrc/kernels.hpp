@@ -446,6 +446,30 @@ __device__ __forceinline__ void seq_phase(int n, int lg, Get get, Put put) {
     }
 }
 
+// The transform descriptor of a band work item, copied to LDS in two steps:
+// desc_fetch issues its global reads into registers, desc_store writes them
+// to LDS. Between the two the kernel issues its router or coefficient reads,
+// so the descriptor's round trip overlaps theirs instead of preceding them.
+template <int NT>
+struct DescCopy {
+    static constexpr int kWords = static_cast<int>(sizeof(FftDesc) / 4);
+    static constexpr int kPer = (kWords + NT - 1) / NT;
+    int w[kPer];
+    __device__ __forceinline__ void fetch(const FftDesc* d) {
+        const int* src = reinterpret_cast<const int*>(d);
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) w[u] = src[min(static_cast<int>(threadIdx.x) + u * NT, kWords - 1)];
+    }
+    __device__ __forceinline__ void store(FftDesc* l) const {
+        int* dst = reinterpret_cast<int*>(l);
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int i = static_cast<int>(threadIdx.x) + u * NT;
+            if (i < kWords) dst[i] = w[u];
+        }
+    }
+};
+
 // Bluestein's middle step on the LDS sequences: v <- conj(v K) for the
 // transformed kernel K (entries 0 .. n-1), sequence sg of this thread.
 template <int NT>
@@ -476,14 +500,14 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
     const WorkItem it = T.items[item0 + blockIdx.x];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
-    const BandDev bd = T.bands[it.band];
-    const FftDesc* fd = T.ffts + bd.fft;
-    // the descriptor in LDS: the stage loop then issues no global loads
+    const BandDev& bd = it.bd;
+    // the descriptor goes to LDS (the stage loop then issues no global
+    // descriptor reads); its read overlaps the router's
     __shared__ FftDesc fdl;
-    for (int i = threadIdx.x; i < static_cast<int>(sizeof(FftDesc) / 4); i += NT)
-        reinterpret_cast<int*>(&fdl)[i] = reinterpret_cast<const int*>(fd)[i];
+    DescCopy<NT> dsc;
+    dsc.fetch(T.ffts + bd.fft);
     float2* buf = lds;
-    const int M = bd.M, n = fd->n;
+    const int M = bd.M, n = bd.n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
     // this thread's sequence; sequences past the item's count read signal 0
@@ -527,6 +551,7 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
     };
     if (blu) route(std::true_type{});
     else route(std::false_type{});
+    dsc.store(&fdl);
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);
@@ -568,13 +593,12 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
     const WorkItem it = T.items[item0 + blockIdx.x];
     const int g = min(it.count, batch - it.s0);
     if (g <= 0) return;
-    const BandDev bd = T.bands[it.band];
-    const FftDesc* fd = T.ffts + bd.fft;
+    const BandDev& bd = it.bd;
     __shared__ FftDesc fdl;
-    for (int i = threadIdx.x; i < static_cast<int>(sizeof(FftDesc) / 4); i += NT)
-        reinterpret_cast<int*>(&fdl)[i] = reinterpret_cast<const int*>(fd)[i];
+    DescCopy<NT> dsc;
+    dsc.fetch(T.ffts + bd.fft);
     float2* buf = lds;
-    const int M = bd.M, n = fd->n;
+    const int M = bd.M, n = bd.n;
     const int lg = it.lgnb, nb = 1 << lg, S = seq_stride(lg);
     const bool blu = bd.chirp >= 0;
     const int sg = threadIdx.x & (nb - 1);
@@ -594,6 +618,7 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
             M, lg, [&](int i) { return at32(cb, crow + i); },
             [&](int i, float2 v) { buf[__mul24(i, S) + sg] = live ? v : make_float2(0.f, 0.f); });
     }
+    dsc.store(&fdl);
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
             buf[__mul24(M + (e >> lg), S) + (e & (nb - 1))] = make_float2(0.f, 0.f);

@@ -176,6 +176,8 @@ struct FftRegistry {
         int64_t Ns = 1, off = 0;
         for (size_t s = 0; s < rad.size(); ++s) {
             const int64_t R = rad[s];
+            d.rcp_ns[s] = static_cast<float>(1.0 / static_cast<double>(Ns));
+            d.rcp_h[s] = R > 16 ? static_cast<float>(1.0 / static_cast<double>((R - 1) / 2)) : 0.0f;
             d.stoff[s] = static_cast<int32_t>(off);
             if (s > 0) {
                 const int64_t stride = n / (Ns * R);
@@ -776,6 +778,7 @@ int finish_plan(HostPlan& p, std::string& err) {
             d.fft = reg.get(M);
             if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no radix plan for a band");
             work[l] = static_cast<int>(M);
+            d.n = static_cast<int32_t>(M);
         } else {
             d.fft = reg.get(P);
             if (d.fft < 0) return fail(err, NSGCQT_EUNSUPPORTED, "no Bluestein length");
@@ -799,6 +802,7 @@ int finish_plan(HostPlan& p, std::string& err) {
             host_dft(bp);
             for (int64_t t = 0; t < P; ++t) push_c(p.kern, bp[t] / static_cast<double>(P));
             work[l] = static_cast<int>(P);
+            d.n = static_cast<int32_t>(P);
             fit[l] = band_fft_fit(P, row_bytes);
         }
         p.banddev.push_back(d);
@@ -881,7 +885,7 @@ int finish_plan(HostPlan& p, std::string& err) {
             const int G = 1 << lg;
             bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg));
             for (int s0 = 0; s0 < batch; s0 += G)
-                p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), lg});
+                p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), lg, p.banddev[static_cast<size_t>(l)]});
         }
         bk.nitems = static_cast<int>(p.items.size()) - bk.item_off;
         if (bk.lds_elems * 8 > 160 * 1024)

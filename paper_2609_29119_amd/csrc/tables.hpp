@@ -46,6 +46,11 @@ struct FftDesc {
     // 64, lane l holding row 16 qb + l % 16 and column 4 kb + l / 16. -1 for
     // other stages.
     int32_t mat[kMaxStages];
+    // per stage: 1 / Ns (the product of the earlier radices) and, for a prime
+    // radix R > 16, 1 / ((R - 1) / 2), rounded once to fp32; the stages'
+    // quotient-and-remainder steps start from these (see Div)
+    float rcp_ns[kMaxStages];
+    float rcp_h[kMaxStages];
 };
 
 // One band of the layout as the band kernels see it.
@@ -58,16 +63,20 @@ struct BandDev {
     int32_t fft;       // FftDesc index: length M, or P for Bluestein
     int32_t chirp;     // -1, or offset of exp(-i pi m^2 / M), m < M, in the chirp pool
     int32_t kern;      // offset of DFT_P(b)/P in the kernel pool (Bluestein only)
+    int32_t n;         // transform length: M, or P for Bluestein
     float inv_M;
 };
 
 // One workgroup of a band kernel: band `band` for signals s0 .. s0 + count - 1,
-// transformed as 2^lgnb interleaved sequences (count <= 2^lgnb).
+// transformed as 2^lgnb interleaved sequences (count <= 2^lgnb). The band's
+// record is repeated here, so a workgroup reads everything it needs to start
+// its loads in one step.
 struct WorkItem {
     int32_t band;
     int32_t s0;
     int32_t count;
     int32_t lgnb;
+    BandDev bd;
 };
 
 // A band whose transform (length M, or Bluestein P) exceeds one workgroup's
