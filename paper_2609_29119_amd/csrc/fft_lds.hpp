@@ -316,6 +316,12 @@ __device__ __forceinline__ void prime_fold(float2* buf, int n, int S, int lgnb, 
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// LDS slot of entry j of a prime stage's root table: the interleave's unused
+// slot in row j (t = nb) for several sequences, or past the data for one.
+// Entries j = 0..R are used (R <= n); the plan sizes the LDS accordingly.
+__device__ __forceinline__ int root_slot0(int n, int S, int lgnb) { return lgnb ? (1 << lgnb) : n; }
+__device__ __forceinline__ int root_step(int S, int lgnb) { return lgnb ? S : 1; }
+
 // Stockham stage for an odd prime radix R (17 <= R <= kMfmaMaxRadix) known
 // only at run time, on the matrix cores. After the fold, the outputs of butterfly column c are
 //   X_q     = y_0 + A_q - i B_q,   X_{R-q} = y_0 + A_q + i B_q,   q = 0..h,
@@ -328,19 +334,31 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 //   im lane: X_q = y0 + A_im - B_re,   X_{R-q} = y0 + A_im + B_re.
 // v_mfma_f32_16x16x4f32 operands: A (16 x 4) lane l row l % 16, column l / 16;
 // B (4 x 16) lane l row l / 16, column l % 16; result (16 x 16) lane l, entry v
-// at row 4 (l / 16) + v, column l % 16. Each wave takes result tiles
+// at row 4 (l / 16) + v, column l % 16. The matrix entries come from the
+// root table omega_R^j = (cos 2 pi j / R, -sin 2 pi j / R), j < R, which the
+// stage copies into LDS (from the length's full root table, stride n / R)
+// while the fold runs: entry (q, r) is omega_R^{q r mod R}, and each lane
+// advances its exponent by 4 q mod R per column block of 4. Entry R holds
+// zero; rows q > h and columns r > h read it. Each wave takes result tiles
 // (column block, row block) round-robin and keeps at most kMfmaTilesPerWave of
 // them until every wave has read its inputs; the caller guarantees
 // mfma_tiles(totb, R) <= kMfmaTilesPerWave * NT / 64.
 template <int NT>
 __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int lgnb, int Ns, int R, float rns,
                                                  float rh, const float2* __restrict__ tws,
-                                                 const float* __restrict__ amat) {
+                                                 const float2* __restrict__ roots) {
     constexpr int NW = NT / 64;
     constexpr int TPW = kMfmaTilesPerWave;
     prime_fold<NT>(buf, n, S, lgnb, Ns, R, rns, rh, tws);
-    __syncthreads();
     const int tid = stage_tid();
+    const int ts = root_step(S, lgnb);
+    float2* tab = buf + root_slot0(n, S, lgnb);
+    {
+        const int stride = n / R;
+        for (int j = tid; j <= R; j += NT)
+            tab[__mul24(j, ts)] = j < R ? at32(roots, static_cast<uint32_t>(__mul24(j, stride))) : make_float2(0.f, 0.f);
+    }
+    __syncthreads();
     const int lane = tid & 63, wave = tid >> 6;
     const int m = n / R;
     const int h = (R - 1) >> 1;
@@ -353,6 +371,7 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
     // least 1/34 from an integer, far beyond the reciprocal's error
     const float rqb = __builtin_amdgcn_rcpf(static_cast<float>(Qb));
     const int kk = lane >> 4, part = lane & 1;
+    const int Rts = __mul24(R, ts);
     float* fb = reinterpret_cast<float*>(buf);
     f32x4 dc[TPW], ds[TPW];
     float y0[TPW];
@@ -367,39 +386,58 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
             const int c = min((cb << 3) + ((lane & 15) >> 1), totb - 1);
             const int a0 = __mul24(c >> lgnb, S) + (c & nbm);
             // s_r.part at input r, d_r.(1 - part) at input R - r (r = 4 kb + kk + 1;
-            // columns past h read inputs that the zero matrix entries cancel)
+            // columns past h read inputs that the zero table entry cancels)
             int as = 2 * (a0 + __mul24(kk + 1, mS)) + part;
             int ad = 2 * (a0 + __mul24(R - kk - 1, mS)) + 1 - part;
             const int step = 8 * mS;
-            const float* ac = amat + qb * Kb * 128 + lane;
-            // four column blocks at a time: all operand reads are issued before
-            // the products that consume them
+            // table exponent of entry (q, r) as a slot offset, and its step per
+            // column block; rows past h sit on the zero entry (step R keeps them there)
+            const int q = (qb << 4) + (lane & 15);
+            int t, inc;
+            if (q <= h) {
+                t = __mul24(q, kk + 1);          // < 2 R
+                t = t >= R ? t - R : t;
+                inc = 4 * q;                      // < 2 R
+                inc = inc >= R ? inc - R : inc;
+                t = __mul24(t, ts);
+                inc = __mul24(inc, ts);
+            } else {
+                t = Rts;
+                inc = Rts;
+            }
+            // all blocks but the last: every column r <= h; two blocks at a
+            // time, their LDS reads issued before the products
             int kb = 0;
-            for (; kb + 4 <= Kb; kb += 4) {
-                float xa[4], xs[4], sv[4], dv[4];
+            for (; kb + 2 < Kb; kb += 2) {
+                float2 w[2];
+                float sv[2], dv[2];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    xa[u] = ac[128 * u];
-                    xs[u] = ac[128 * u + 64];
+                for (int u = 0; u < 2; ++u) {
+                    w[u] = tab[t];
                     sv[u] = fb[as + u * step];
                     dv[u] = fb[ad - u * step];
+                    const uint32_t nx = static_cast<uint32_t>(t + inc);
+                    t = static_cast<int>(min(nx, nx - static_cast<uint32_t>(Rts)));
                 }
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    dc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa[u], sv[u], dc[i], 0, 0, 0);
-                    ds[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xs[u], dv[u], ds[i], 0, 0, 0);
+                for (int u = 0; u < 2; ++u) {
+                    dc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[u].x, sv[u], dc[i], 0, 0, 0);
+                    ds[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[u].y, dv[u], ds[i], 0, 0, 0);
                 }
-                as += 4 * step;
-                ad -= 4 * step;
-                ac += 512;
+                as += 2 * step;
+                ad -= 2 * step;
             }
             for (; kb < Kb; ++kb) {
-                const float xa = ac[0], xs = ac[64], sv = fb[as], dv = fb[ad];
-                dc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xa, sv, dc[i], 0, 0, 0);
-                ds[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(xs, dv, ds[i], 0, 0, 0);
+                // in the last block, columns r = 4 kb + kk + 1 > h read the zero entry
+                const int tu = (kb == Kb - 1 && 4 * kb + kk + 1 > h) ? Rts : t;
+                const float2 w = tab[tu];
+                const float sv = fb[as], dv = fb[ad];
+                dc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(w.x, sv, dc[i], 0, 0, 0);
+                ds[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(w.y, dv, ds[i], 0, 0, 0);
                 as += step;
                 ad -= step;
-                ac += 128;
+                const uint32_t nx = static_cast<uint32_t>(t + inc);
+                t = static_cast<int>(min(nx, nx - static_cast<uint32_t>(Rts)));
             }
             y0[i] = fb[2 * a0 + part];
         }
@@ -417,7 +455,8 @@ __device__ __forceinline__ void stage_prime_mfma(float2* buf, int n, int S, int 
                 int k = 0;
                 if (Ns > 1) qdiv(jj, dns, k);
                 const int ob = 2 * (__mul24(__mul24(jj - k, R) + k, S) + t) + part;
-                const float sg = part ? -1.f : 1.f;
+                // the table holds -sin: B = -(sine product)
+                const float sg = part ? 1.f : -1.f;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int q = (qb << 4) + 4 * kk + v;
@@ -468,8 +507,7 @@ __device__ __forceinline__ void lds_fft(float2* buf, int S, int lgnb, const FftD
             case 15: stage_fixed<15, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
             case 16: stage_fixed<16, NT, EPT>(buf, n, S, lgnb, Ns, rns, tw); break;
             default:
-                stage_prime_mfma<NT>(buf, n, S, lgnb, Ns, R, rns, d->rcp_h[s], tw,
-                                     reinterpret_cast<const float*>(pool + d->mat[s]));
+                stage_prime_mfma<NT>(buf, n, S, lgnb, Ns, R, rns, d->rcp_h[s], tw, pool + d->full);
                 break;
         }
         Ns *= R;

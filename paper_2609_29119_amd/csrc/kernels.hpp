@@ -17,6 +17,9 @@
 
 #include "fft_lds.hpp"
 
+#ifndef NSG_RU
+#define NSG_RU 4
+#endif
 namespace nsg {
 
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
@@ -549,8 +552,57 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                 buf[__mul24(slot, S) + sg] = v;
             });
     };
-    if (blu) route(std::true_type{});
-    else route(std::false_type{});
+    // The same for a band inside 0 < k < L whose reads past its last entry
+    // stay inside the workspace and table guards (the plan's item flag): the
+    // entries i = i0 + j st of a thread are read through addresses affine in
+    // j, four at a time, without clamps; entries past M are read but not
+    // used. The slot of entry i advances by st modulo M.
+    auto route_fast = [&](auto blu_t) {
+        constexpr bool BLU = decltype(blu_t)::value;
+        constexpr int RU = NSG_RU;
+        const int st = NT >> lg, i0 = static_cast<int>(threadIdx.x) >> lg;
+        const int wl = live ? bd.W : 0;
+        int slot = i0 + bd.rot;
+        slot = slot >= M ? slot - M : slot;
+        uint32_t zo = zrow + static_cast<uint32_t>(bd.k_lo + i0);
+        uint32_t mo = zrow + static_cast<uint32_t>(L - bd.k_lo - i0);
+        for (int ib = i0; ib < M; ib += RU * st) {
+            float2 za[RU], zb[RU], ch[RU];
+            float4 r[RU];
+            int sl[RU];
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                za[u] = at32(Zb + u * st, zo);
+                zb[u] = at32(Zb - u * st, mo);
+                r[u] = at32(rb + u * st, static_cast<uint32_t>(ib));
+                sl[u] = slot;
+                if (BLU) ch[u] = at32(chb, static_cast<uint32_t>(slot));
+                const uint32_t nx = static_cast<uint32_t>(slot + st);
+                slot = static_cast<int>(min(nx, nx - static_cast<uint32_t>(M)));
+            }
+            zo += RU * st;
+            mo -= RU * st;
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                const int i = ib + u * st;
+                if (i < M) {
+                    // conj(u), u = (1/2) w (1 - i w_k) Z_a + (1/2) w (1 + i w_k) conj(Z_b)
+                    float2 v = make_float2(r[u].x * za[u].x - r[u].y * za[u].y + r[u].z * zb[u].x + r[u].w * zb[u].y,
+                                           -(r[u].x * za[u].y + r[u].y * za[u].x) - r[u].w * zb[u].x + r[u].z * zb[u].y);
+                    if (BLU) v = cmul(v, ch[u]);
+                    if (i >= wl) v = make_float2(0.f, 0.f);
+                    buf[__mul24(sl[u], S) + sg] = v;
+                }
+            }
+        }
+    };
+    if (it.fast & kItemFastRoute) {
+        if (blu) route_fast(std::true_type{});
+        else route_fast(std::false_type{});
+    } else {
+        if (blu) route(std::true_type{});
+        else route(std::false_type{});
+    }
     dsc.store(&fdl);
     if (blu)
         for (int e = threadIdx.x; e < ((n - M) << lg); e += NT)
@@ -573,9 +625,20 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                 at32(cb, crow + i) = cscale(cmul(conjf2(chi), buf[__mul24(i, S) + sg]), bd.inv_M);
             });
     } else {
-        for (int i = threadIdx.x >> lg; i < M; i += NT >> lg) {
-            const float2 v = buf[__mul24(i, S) + sg];
-            at32(cb, crow + i) = make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+        // four entries i = ib + j st at a time: the global addresses are
+        // affine in j (scalar base, one lane offset)
+        const int st = NT >> lg, i0 = static_cast<int>(threadIdx.x) >> lg;
+        const int stS = __mul24(st, S);
+        int a = __mul24(i0, S) + sg;
+        for (int ib = i0; ib < M; ib += 4 * st) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (ib + u * st < M) {
+                    const float2 v = buf[a + u * stS];
+                    at32(cb + u * st, crow + static_cast<uint32_t>(ib)) = make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+                }
+            }
+            a += 4 * stS;
         }
     }
 }

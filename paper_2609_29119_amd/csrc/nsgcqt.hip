@@ -137,11 +137,14 @@ int upload(nsgcqt_plan_s* p) {
     struct Chunk { const void* src; int64_t bytes; int64_t off; };
     std::vector<Chunk> ch;
     int64_t total = 0;
-    auto add = [&](const void* src, int64_t bytes) {
+    // guard: bytes after the table that the band kernels' fast load phases
+    // may read (and ignore)
+    auto add = [&](const void* src, int64_t bytes, int64_t guard = 0) {
         ch.push_back({src, bytes, total});
-        total += align256(bytes > 0 ? bytes : 1);
+        total += align256((bytes > 0 ? bytes : 1) + guard);
         return ch.size() - 1;
     };
+    const int64_t g1 = kFastGuard * static_cast<int64_t>(sizeof(float)), g4 = 4 * g1;
     const size_t iBands = add(h.banddev.data(), h.banddev.size() * sizeof(BandDev));
     const size_t iFfts = add(h.ffts.data(), h.ffts.size() * sizeof(FftDesc));
     const size_t iTw = add(h.twpool.data(), h.twpool.size() * sizeof(float));
@@ -157,12 +160,12 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iItems = add(h.items.data(), h.items.size() * sizeof(WorkItem));
     const size_t iBigs = add(h.bigs.data(), h.bigs.size() * sizeof(BigDesc));
     const size_t iBigItems = add(h.bigitems.data(), h.bigitems.size() * sizeof(BigItem));
-    const size_t iWA = add(h.wA.data(), h.wA.size() * sizeof(float));
-    const size_t iWS = add(h.wS.data(), h.wS.size() * sizeof(float));
-    const size_t iWT = add(h.wT.data(), h.wT.size() * sizeof(float));
-    const size_t iWSa = add(h.wSa.data(), h.wSa.size() * sizeof(float));
-    const size_t iRA = add(h.rA.data(), h.rA.size() * sizeof(float));
-    const size_t iRSa = add(h.rSa.data(), h.rSa.size() * sizeof(float));
+    const size_t iWA = add(h.wA.data(), h.wA.size() * sizeof(float), g1);
+    const size_t iWS = add(h.wS.data(), h.wS.size() * sizeof(float), g1);
+    const size_t iWT = add(h.wT.data(), h.wT.size() * sizeof(float), g1);
+    const size_t iWSa = add(h.wSa.data(), h.wSa.size() * sizeof(float), g1);
+    const size_t iRA = add(h.rA.data(), h.rA.size() * sizeof(float), g4);
+    const size_t iRSa = add(h.rSa.data(), h.rSa.size() * sizeof(float), g4);
 
     HIP_TRY(hipGetDevice(&p->dev));
     char* d = nullptr;

@@ -200,6 +200,10 @@ int fail(std::string& err, int code, const std::string& msg) {
     return code;
 }
 
+// Tiles a four-step pass aims for at least: 2.5 per compute unit of MI355X
+// (256 CUs), so that the last round of a persistent pass is not a long tail.
+constexpr int64_t kPassTiles = 640;
+
 // Band kernel tiers by transform length: threads and elements per thread.
 struct Tier { int max_work, nt, ept; };
 constexpr Tier kTiers[] = {{512, 64, 8}, {2048, 256, 8}, {4096, 256, 16}, {8192, 512, 16}, {16384, 1024, 16}};
@@ -703,10 +707,15 @@ int finish_plan(HostPlan& p, std::string& err) {
         f.fft1 = reg.get(f.L1);
         f.fft2 = reg.get(f.L2);
         // up to 16 sequences per workgroup (a power of two), at most 8
-        // elements per thread
-        auto pick = [](int64_t n, int64_t count, int& lgt, int& nt) {
+        // elements per thread; fewer (down to 2) while the pass would have
+        // fewer than kPassTiles tiles, so that small batches still spread
+        // over the device (each sequence's arithmetic does not depend on
+        // how many share a workgroup)
+        const int64_t nsig = batch;
+        auto pick = [nsig](int64_t n, int64_t count, int& lgt, int& nt) {
             lgt = 4;
             while (lgt > 0 && ((int64_t(1) << lgt) * n > 8192 || (int64_t(1) << (lgt - 1)) >= count)) --lgt;
+            while (lgt > 1 && ((count + (int64_t(1) << lgt) - 1) >> lgt) * nsig < kPassTiles) --lgt;
             nt = 1024;
             for (int t : {256, 512, 1024})
                 if ((int64_t(1) << lgt) * n <= 8 * t) { nt = t; break; }
@@ -884,8 +893,18 @@ int finish_plan(HostPlan& p, std::string& err) {
             const int lg = std::min(seq_lg(n, E, batch, row_bytes), fit[l].lg_cap);
             const int G = 1 << lg;
             bk.lds_elems = std::max(bk.lds_elems, lds_slots(n, lg));
+            // fast load phases (WorkItem flags): every read up to entry
+            // M - 1 + 3 st of the band stays in the data or the guards
+            const auto& hb = p.bands[static_cast<size_t>(l)];
+            const int64_t st = bk.nt >> lg, reach = hb.M - 1 + 3 * st;
+            int32_t fast = 0;
+            if (hb.k_lo >= 1 && hb.k_lo + hb.M <= L && hb.k_lo + reach < L + kFastGuard && 3 * st <= L &&
+                hb.off + reach < p.C + kFastGuard)
+                fast |= kItemFastRoute;
+            if (hb.off + reach < p.C) fast |= kItemFastCoef;
             for (int s0 = 0; s0 < batch; s0 += G)
-                p.items.push_back(WorkItem{l, s0, std::min(G, batch - s0), lg, p.banddev[static_cast<size_t>(l)]});
+                p.items.push_back(
+                    WorkItem{l, s0, std::min(G, batch - s0), lg, fast, p.banddev[static_cast<size_t>(l)]});
         }
         bk.nitems = static_cast<int>(p.items.size()) - bk.item_off;
         if (bk.lds_elems * 8 > 160 * 1024)
@@ -927,7 +946,9 @@ int finish_plan(HostPlan& p, std::string& err) {
     // ---- workspace
     const int64_t b = batch;
     const int64_t hbytes = p.Hn ? 2 * align256(8 * p.Hn * b) : 0;
-    p.off_h_an = 2 * align256(8 * L * b);
+    // the packed spectrum is followed by a guard for the band kernels' fast
+    // router reads (kFastGuard entries)
+    p.off_h_an = align256(8 * L * b) + align256(8 * L * b + 8 * static_cast<int64_t>(kFastGuard));
     p.ws_an = p.off_h_an + hbytes;
     p.off_h_syn = align256(8 * p.C * b) + align256(8 * L * b);
     p.off_y_sliced = p.off_h_syn + hbytes;

@@ -76,8 +76,19 @@ struct WorkItem {
     int32_t s0;
     int32_t count;
     int32_t lgnb;
+    int32_t fast;      // kItemFast* flags
     BandDev bd;
 };
+
+// Work item flags. A band kernel's fast load phases read entries up to
+// kFastReach(M, st) = M - 1 + 3 st past the band's first one (st = threads per
+// sequence) through affine addresses; the plan sets a flag only where every
+// such read stays inside the data, the workspace guard or the table guard.
+constexpr int32_t kItemFastRoute = 1;    // analysis router: 0 < k < L, Z and router tables
+constexpr int32_t kItemFastCoef = 2;     // synthesis: coefficient reads stay inside the row set
+// Guard, in complex entries, after the packed spectrum in the analysis
+// workspace and after the per-coefficient tables.
+constexpr int kFastGuard = 4096;
 
 // A band whose transform (length M, or Bluestein P) exceeds one workgroup's
 // LDS: it is transformed by a four-step FFT n = n1 * n2 through a per-signal
@@ -100,7 +111,25 @@ struct BigItem {
     int32_t pad;
 };
 
-// LDS slots of nb = 2^lgnb interleaved sequences of length n (stride nb + 1).
-inline int lds_slots(int n, int lgnb) { return lgnb ? n * ((1 << lgnb) + 1) : n; }
+// Largest prime factor of n above 16 (the radix of a matrix-core stage), or 0.
+inline int mfma_prime(int n) {
+    int best = 0;
+    for (int p = 2; p * p <= n; ++p)
+        while (n % p == 0) {
+            if (p > 16) best = p;
+            n /= p;
+        }
+    return n > 16 && n > best ? n : best;
+}
+
+// LDS slots of nb = 2^lgnb interleaved sequences of length n (stride nb + 1),
+// with room for a matrix-core stage's root table (entries 0..R): the unused
+// slot of each row (plus one row when R = n), or R + 1 slots after a single
+// sequence.
+inline int lds_slots(int n, int lgnb) {
+    const int R = mfma_prime(n);
+    if (lgnb) return (R == n ? n + 1 : n) * ((1 << lgnb) + 1);
+    return n + (R ? R + 1 : 0);
+}
 
 }  // namespace nsg
