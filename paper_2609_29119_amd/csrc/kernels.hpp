@@ -17,9 +17,6 @@
 
 #include "fft_lds.hpp"
 
-#ifndef NSG_RU
-#define NSG_RU 4
-#endif
 namespace nsg {
 
 // Ask for at least two waves per SIMD so LDS-bound stages can overlap; this
@@ -449,6 +446,27 @@ __device__ __forceinline__ void seq_phase(int n, int lg, Get get, Put put) {
     }
 }
 
+// Two consecutive complex values at element idx of base (a 16-byte access;
+// idx need not be even: global accesses only need dword alignment).
+__device__ __forceinline__ float4 ld2c(const float2* base, uint32_t idx) {
+    return *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(base) + idx * 8u);
+}
+__device__ __forceinline__ void st2c(float2* base, uint32_t idx, float4 v) {
+    *reinterpret_cast<float4*>(reinterpret_cast<char*>(base) + idx * 8u) = v;
+}
+
+// The router's value for one entry (eq. 7): conj(u) with
+// u = (1/2) w (1 - i w_k) Z_a + (1/2) w (1 + i w_k) conj(Z_b), r holding the two
+// factors. Every load form of the router goes through this one expression,
+// so the result bits do not depend on which form a work item takes.
+// Written as explicit fused multiply-adds, so the compiler cannot contract
+// it differently in different places.
+__device__ __forceinline__ float2 route_value(float4 r, float2 za, float2 zb) {
+    const float ux = fmaf(r.x, za.x, fmaf(-r.y, za.y, fmaf(r.z, zb.x, r.w * zb.y)));
+    const float uy = fmaf(r.x, za.y, fmaf(r.y, za.x, fmaf(-r.z, zb.y, r.w * zb.x)));
+    return make_float2(ux, -uy);
+}
+
 // The transform descriptor of a band work item, copied to LDS in two steps:
 // desc_fetch issues its global reads into registers, desc_store writes them
 // to LDS. Between the two the kernel issues its router or coefficient reads,
@@ -543,56 +561,65 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                 if (slot >= M) slot -= M;
                 float2 v = make_float2(0.f, 0.f);
                 if (live && i < bd.W) {
-                    // u = (1/2) w (1 - i w_k) Z_a + (1/2) w (1 + i w_k) conj(Z_b)
-                    const float2 u = cadd(cmul(make_float2(r.r.x, r.r.y), r.za),
-                                          cmul(make_float2(r.r.z, r.r.w), conjf2(r.zb)));
-                    v = conjf2(u);
+                    v = route_value(r.r, r.za, r.zb);
                     if (BLU) v = cmul(v, r.ch);
                 }
                 buf[__mul24(slot, S) + sg] = v;
             });
     };
     // The same for a band inside 0 < k < L whose reads past its last entry
-    // stay inside the workspace and table guards (the plan's item flag): the
-    // entries i = i0 + j st of a thread are read through addresses affine in
-    // j, four at a time, without clamps; entries past M are read but not
-    // used. The slot of entry i advances by st modulo M.
+    // stay inside the workspace and table guards (the plan's item flag). A
+    // thread takes pairs of entries (i, i + 1), i = 2 (p0 + j st): one
+    // 16-byte read of Z_k, Z_{k+1}, one of the mirror pair Z_{L-k-1},
+    // Z_{L-k} and two of the router factors, all at addresses affine in j;
+    // entries past M are read but not used. The slot of entry i advances
+    // by 2 st modulo M.
     auto route_fast = [&](auto blu_t) {
         constexpr bool BLU = decltype(blu_t)::value;
-        constexpr int RU = NSG_RU;
-        const int st = NT >> lg, i0 = static_cast<int>(threadIdx.x) >> lg;
+        constexpr int RP = 2;                     // pairs per batch
+        const int st = NT >> lg, p0 = static_cast<int>(threadIdx.x) >> lg;
         const int wl = live ? bd.W : 0;
-        int slot = i0 + bd.rot;
+        const int st2 = 2 * st;
+        int slot = 2 * p0 + bd.rot;               // < 2 M whenever 2 p0 < M
         slot = slot >= M ? slot - M : slot;
-        uint32_t zo = zrow + static_cast<uint32_t>(bd.k_lo + i0);
-        uint32_t mo = zrow + static_cast<uint32_t>(L - bd.k_lo - i0);
-        for (int ib = i0; ib < M; ib += RU * st) {
-            float2 za[RU], zb[RU], ch[RU];
-            float4 r[RU];
-            int sl[RU];
+        uint32_t zo = zrow + static_cast<uint32_t>(bd.k_lo + 2 * p0);
+        uint32_t mo = zrow + static_cast<uint32_t>(L - bd.k_lo - 2 * p0 - 1);
+        for (int ib = 2 * p0; ib < M; ib += RP * st2) {
+            float4 za[RP], zb[RP], r0[RP], r1[RP];
+            float2 c0[RP], c1[RP];
+            int sl[RP];
 #pragma unroll
-            for (int u = 0; u < RU; ++u) {
-                za[u] = at32(Zb + u * st, zo);
-                zb[u] = at32(Zb - u * st, mo);
-                r[u] = at32(rb + u * st, static_cast<uint32_t>(ib));
+            for (int u = 0; u < RP; ++u) {
+                za[u] = ld2c(Zb + u * st2, zo);
+                zb[u] = ld2c(Zb - u * st2, mo);
+                r0[u] = at32(rb + u * st2, static_cast<uint32_t>(ib));
+                r1[u] = at32(rb + u * st2 + 1, static_cast<uint32_t>(ib));
                 sl[u] = slot;
-                if (BLU) ch[u] = at32(chb, static_cast<uint32_t>(slot));
-                const uint32_t nx = static_cast<uint32_t>(slot + st);
+                if (BLU) {
+                    const int s1 = slot + 1 == M ? 0 : slot + 1;
+                    c0[u] = at32(chb, static_cast<uint32_t>(slot));
+                    c1[u] = at32(chb, static_cast<uint32_t>(s1));
+                }
+                const uint32_t nx = static_cast<uint32_t>(slot + st2);
                 slot = static_cast<int>(min(nx, nx - static_cast<uint32_t>(M)));
             }
-            zo += RU * st;
-            mo -= RU * st;
+            zo += RP * st2;
+            mo -= RP * st2;
 #pragma unroll
-            for (int u = 0; u < RU; ++u) {
-                const int i = ib + u * st;
-                if (i < M) {
-                    // conj(u), u = (1/2) w (1 - i w_k) Z_a + (1/2) w (1 + i w_k) conj(Z_b)
-                    float2 v = make_float2(r[u].x * za[u].x - r[u].y * za[u].y + r[u].z * zb[u].x + r[u].w * zb[u].y,
-                                           -(r[u].x * za[u].y + r[u].y * za[u].x) - r[u].w * zb[u].x + r[u].z * zb[u].y);
-                    if (BLU) v = cmul(v, ch[u]);
-                    if (i >= wl) v = make_float2(0.f, 0.f);
-                    buf[__mul24(sl[u], S) + sg] = v;
+            for (int u = 0; u < RP; ++u) {
+                const int i = ib + u * st2;
+                // entry i: Z_k = za.xy, Z_{L-k} = zb.zw; entry i + 1: za.zw, zb.xy
+                float2 v0 = route_value(r0[u], make_float2(za[u].x, za[u].y), make_float2(zb[u].z, zb[u].w));
+                float2 v1 = route_value(r1[u], make_float2(za[u].z, za[u].w), make_float2(zb[u].x, zb[u].y));
+                if (BLU) {
+                    v0 = cmul(v0, c0[u]);
+                    v1 = cmul(v1, c1[u]);
                 }
+                if (i >= wl) v0 = make_float2(0.f, 0.f);
+                if (i + 1 >= wl) v1 = make_float2(0.f, 0.f);
+                const int s1 = sl[u] + 1 == M ? 0 : sl[u] + 1;
+                if (i < M) buf[__mul24(sl[u], S) + sg] = v0;
+                if (i + 1 < M) buf[__mul24(s1, S) + sg] = v1;
             }
         }
     };
@@ -625,20 +652,26 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_analysis(const float2*
                 at32(cb, crow + i) = cscale(cmul(conjf2(chi), buf[__mul24(i, S) + sg]), bd.inv_M);
             });
     } else {
-        // four entries i = ib + j st at a time: the global addresses are
-        // affine in j (scalar base, one lane offset)
-        const int st = NT >> lg, i0 = static_cast<int>(threadIdx.x) >> lg;
-        const int stS = __mul24(st, S);
-        int a = __mul24(i0, S) + sg;
-        for (int ib = i0; ib < M; ib += 4 * st) {
+        // pairs of entries (i, i + 1), i = 2 (p0 + j st), two at a time: one
+        // 16-byte write per pair at addresses affine in j (scalar base, one
+        // lane offset); a lone last entry is written on its own
+        const int st = NT >> lg, p0 = static_cast<int>(threadIdx.x) >> lg;
+        const int st2 = 2 * st, stS = __mul24(st2, S);
+        int a = __mul24(2 * p0, S) + sg;
+        for (int ib = 2 * p0; ib < M; ib += 2 * st2) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                if (ib + u * st < M) {
-                    const float2 v = buf[a + u * stS];
-                    at32(cb + u * st, crow + static_cast<uint32_t>(ib)) = make_float2(v.x * bd.inv_M, -v.y * bd.inv_M);
+            for (int u = 0; u < 2; ++u) {
+                const int i = ib + u * st2;
+                if (i + 1 < M) {
+                    const float2 v0 = buf[a + u * stS], v1 = buf[a + u * stS + S];
+                    st2c(cb + u * st2, crow + static_cast<uint32_t>(ib),
+                         make_float4(v0.x * bd.inv_M, -v0.y * bd.inv_M, v1.x * bd.inv_M, -v1.y * bd.inv_M));
+                } else if (i < M) {
+                    const float2 v0 = buf[a + u * stS];
+                    at32(cb + u * st2, crow + static_cast<uint32_t>(ib)) = make_float2(v0.x * bd.inv_M, -v0.y * bd.inv_M);
                 }
             }
-            a += 4 * stS;
+            a += 2 * stS;
         }
     }
 }
@@ -782,7 +815,7 @@ __global__ __launch_bounds__(NT) NSG_OCC void k_big_a(BigArgs a, Tables T, int i
                         const int kb = (ka == 0) ? 0 : a.L - ka;
                         const float2 za = Zs[ka], zb = Zs[kb];
                         const float4 r = a.rt[bd.off + i];             // router factors
-                        v = conjf2(cadd(cmul(make_float2(r.x, r.y), za), cmul(make_float2(r.z, r.w), conjf2(zb))));
+                        v = route_value(r, za, zb);
                     }
                 } else {
                     v = a.cin[(long long)it.sig * a.C + bd.off + j];
