@@ -702,7 +702,40 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
     const float2* chb = T.chirp + (blu ? bd.chirp : 0);   // entry 0 is valid in every table
     const float2* cb = coef + (long long)it.s0 * C + bd.off;
     const uint32_t crow = static_cast<uint32_t>(live ? sg : 0) * static_cast<uint32_t>(C);
-    if (blu) {
+    // fast form (the plan's item flag: reads up to entry M + 2 st stay in the
+    // row): pairs of entries (i, i + 1), i = 2 (p0 + j st), one 16-byte read
+    // of the coefficients each (and of the chirp for Bluestein)
+    auto load_fast = [&](auto blu_t) {
+        constexpr bool BLU = decltype(blu_t)::value;
+        const int st = NT >> lg, p0 = static_cast<int>(threadIdx.x) >> lg;
+        const int st2 = 2 * st, stS = __mul24(st2, S);
+        int a = __mul24(2 * p0, S) + sg;
+        for (int ib = 2 * p0; ib < M; ib += 2 * st2) {
+            float4 cv[2], hv[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                cv[u] = ld2c(cb + u * st2, crow + static_cast<uint32_t>(ib));
+                if (BLU) hv[u] = ld2c(chb + u * st2, static_cast<uint32_t>(ib));
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int i = ib + u * st2;
+                float2 v0 = make_float2(cv[u].x, cv[u].y), v1 = make_float2(cv[u].z, cv[u].w);
+                if (BLU) {
+                    v0 = cmul(v0, make_float2(hv[u].x, hv[u].y));
+                    v1 = cmul(v1, make_float2(hv[u].z, hv[u].w));
+                }
+                if (!live) v0 = v1 = make_float2(0.f, 0.f);
+                if (i < M) buf[a + u * stS] = v0;
+                if (i + 1 < M) buf[a + u * stS + S] = v1;
+            }
+            a += 2 * stS;
+        }
+    };
+    if (it.fast & kItemFastCoef) {
+        if (blu) load_fast(std::true_type{});
+        else load_fast(std::false_type{});
+    } else if (blu) {
         seq_phase<NT, 4>(
             M, lg, [&](int i) { return make_float4_2(at32(cb, crow + i), at32(chb, i)); },
             [&](int i, float4 r) {
@@ -746,8 +779,47 @@ __global__ __launch_bounds__(NT) NSG_OCC_BAND void k_band_synthesis(const float2
                 at32(Wb, crow + i) = cscale(u, r.w);
             });
     };
-    if (blu) weigh(std::true_type{});
-    else weigh(std::false_type{});
+    // pairs of support entries (i, i + 1), i = 2 (p0 + j st): one 8-byte read
+    // of the weights and one 16-byte write of W per pair (the weight table's
+    // guard covers the reads past the support)
+    auto weigh_fast = [&](auto blu_t) {
+        constexpr bool BLU = decltype(blu_t)::value;
+        const int st = NT >> lg, p0 = static_cast<int>(threadIdx.x) >> lg;
+        const int st2 = 2 * st, Wd = bd.W;
+        int slot = 2 * p0 + bd.rot;               // < 2 M whenever 2 p0 < W
+        slot = slot >= M ? slot - M : slot;
+        for (int ib = 2 * p0; ib < Wd; ib += 2 * st2) {
+            float2 wv[2], h0[2], h1[2];
+            int sl[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                wv[u] = *reinterpret_cast<const float2*>(w + u * st2 + ib);
+                sl[u] = slot;
+                if (BLU) {
+                    h0[u] = at32(chb, static_cast<uint32_t>(slot));
+                    h1[u] = at32(chb, static_cast<uint32_t>(slot + 1 == M ? 0 : slot + 1));
+                }
+                const uint32_t nx = static_cast<uint32_t>(slot + st2);
+                slot = static_cast<int>(min(nx, nx - static_cast<uint32_t>(M)));
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int i = ib + u * st2;
+                const int s1 = sl[u] + 1 == M ? 0 : sl[u] + 1;
+                float2 u0 = buf[__mul24(sl[u], S) + sg], u1 = buf[__mul24(s1, S) + sg];
+                if (BLU) {
+                    u0 = cmul(h0[u], conjf2(u0));
+                    u1 = cmul(h1[u], conjf2(u1));
+                }
+                u0 = cscale(u0, wv[u].x);
+                u1 = cscale(u1, wv[u].y);
+                if (i + 1 < Wd) st2c(Wb + u * st2, crow + static_cast<uint32_t>(ib), make_float4_2(u0, u1));
+                else if (i < Wd) at32(Wb + u * st2, crow + static_cast<uint32_t>(ib)) = u0;
+            }
+        }
+    };
+    if (blu) weigh_fast(std::true_type{});
+    else weigh_fast(std::false_type{});
 }
 
 // ------------------------------------------------------------ huge bands

@@ -152,7 +152,7 @@ int upload(nsgcqt_plan_s* p) {
     const size_t iOwn = add(h.owner.data(), h.owner.size() * sizeof(int32_t));
     const size_t iBase = add(h.bandbase.data(), h.bandbase.size() * sizeof(int32_t));
     const size_t iGather = add(h.gather.data(), h.gather.size() * sizeof(int32_t));
-    const size_t iCh = add(h.chirp.data(), h.chirp.size() * sizeof(float));
+    const size_t iCh = add(h.chirp.data(), h.chirp.size() * sizeof(float), 2 * g1);
     const size_t iK = add(h.kern.data(), h.kern.size() * sizeof(float));
     const size_t iHi = add(h.tw4_hi.data(), h.tw4_hi.size() * sizeof(float));
     const size_t iLo = add(h.tw4_lo.data(), h.tw4_lo.size() * sizeof(float));
