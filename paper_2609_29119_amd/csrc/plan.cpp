@@ -123,31 +123,7 @@ namespace {
 struct FftRegistry {
     HostPlan& p;
     std::map<int64_t, int> index;
-    std::map<int, int32_t> mats;   // prime radix -> offset of its matrix fragments
     explicit FftRegistry(HostPlan& plan) : p(plan) {}
-
-    // Matrix-core fragments of the cosine and sine matrices of prime R (layout
-    // in FftDesc::mat), angles reduced exactly: (q r) mod R.
-    int32_t matrix(int R) {
-        auto it = mats.find(R);
-        if (it != mats.end()) return it->second;
-        const int h = (R - 1) / 2, Qb = (h + 16) >> 4, Kb = (h + 3) >> 2;
-        const int32_t off = static_cast<int32_t>(p.twpool.size() / 2);
-        for (int qb = 0; qb < Qb; ++qb)
-            for (int kb = 0; kb < Kb; ++kb)
-                for (int which = 0; which < 2; ++which)
-                    for (int l = 0; l < 64; ++l) {
-                        const int q = 16 * qb + l % 16, r = 4 * kb + l / 16 + 1;
-                        double v = 0.0;
-                        if (q <= h && r <= h) {
-                            const double ang = 2.0 * kPi * static_cast<double>((q * r) % R) / R;
-                            v = which ? std::sin(ang) : std::cos(ang);
-                        }
-                        p.twpool.push_back(static_cast<float>(v));
-                    }
-        mats[R] = off;
-        return off;
-    }
 
     // Index of the FftDesc for length n, creating it (and its twiddles) on
     // first use; -1 if n does not factor into supported radices.
@@ -159,10 +135,7 @@ struct FftRegistry {
         FftDesc d{};
         d.n = static_cast<int32_t>(n);
         d.nstages = static_cast<int32_t>(rad.size());
-        for (size_t s = 0; s < rad.size(); ++s) {
-            d.radix[s] = static_cast<int16_t>(rad[s]);
-            d.mat[s] = rad[s] > 16 ? matrix(rad[s]) : -1;
-        }
+        for (size_t s = 0; s < rad.size(); ++s) d.radix[s] = static_cast<int16_t>(rad[s]);
         d.full = static_cast<int32_t>(p.twpool.size() / 2);
         for (int64_t t = 0; t < n; ++t) push_c(p.twpool, root(t, n));
         int lg = 0;

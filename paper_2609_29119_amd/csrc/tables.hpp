@@ -38,14 +38,6 @@ struct FftDesc {
     int32_t ntw;
     int16_t radix[kMaxStages];
     int32_t stoff[kMaxStages];
-    // per stage with a prime radix R > 16: pool offset (in complex entries) of
-    // the matrix-core fragments of cos(2 pi q r / R) and sin(2 pi q r / R),
-    // rows q = 0..h, columns r = 1..h (h = (R - 1) / 2), zero-padded to
-    // Qb = (h + 16) / 16 row blocks of 16 and Kb = (h + 3) / 4 column blocks of
-    // 4; fragment (qb, kb, which) holds 64 floats at ((qb Kb + kb) 2 + which)
-    // 64, lane l holding row 16 qb + l % 16 and column 4 kb + l / 16. -1 for
-    // other stages.
-    int32_t mat[kMaxStages];
     // per stage: 1 / Ns (the product of the earlier radices) and, for a prime
     // radix R > 16, 1 / ((R - 1) / 2), rounded once to fp32; the stages'
     // quotient-and-remainder steps start from these (see Div)
