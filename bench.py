@@ -430,11 +430,18 @@ def time_calls(plan, calls, K, W, use_ev=True):
     algb = [b for st in infos for _, b in st]
     nev = [2 * len(st) for st in infos]          # a start and an end event per kernel
 
+    armed = [True]      # whether the library may still hold stage events
+
     def step(evs=None):
         for i, (_, f) in enumerate(calls):
-            plan.set_stage_events(None if evs is None else evs[i])
+            e = None if evs is None else evs[i]
+            if e is not None or armed[0]:
+                plan.set_stage_events(e)
+                armed[0] = e is not None
             f()
-        plan.set_stage_events(None)
+        if armed[0]:
+            plan.set_stage_events(None)
+            armed[0] = False
 
     for _ in range(W):
         step()
@@ -464,17 +471,23 @@ def time_calls(plan, calls, K, W, use_ev=True):
         dom = int(np.argmax(dur))
     evd = HipEvents(2 * K) if dom is not None else None
 
+    # the timed steps' event arguments, built before the timed region: only
+    # the call holding the dominant kernel brackets it, the others record none
+    timed_evs = []
+    if evd is not None:
+        for i in range(K):
+            j, evs = dom, []
+            for n in nev:
+                if 0 <= j < n // 2:
+                    lst = [None] * (2 * j) + [evd.ev[2 * i], evd.ev[2 * i + 1]]
+                    evs.append((ctypes.c_void_p * len(lst))(*lst))
+                else:
+                    evs.append(None)
+                j -= n // 2
+            timed_evs.append(evs)
+
     def timed_step(i):
-        if evd is None:
-            return step()
-        j, evs = dom, []
-        for n in nev:
-            if 0 <= j < n // 2:
-                evs.append([None] * (2 * j) + [evd.ev[2 * i], evd.ev[2 * i + 1]])
-            else:
-                evs.append(None)
-            j -= n // 2
-        step(evs)
+        step(timed_evs[i] if timed_evs else None)
 
     t_start = torch.cuda.Event(enable_timing=True)
     t_stop = torch.cuda.Event(enable_timing=True)

@@ -46,21 +46,22 @@ __device__ __forceinline__ int stage_tid() {
     return t;
 }
 
-// Exact quotient and remainder of 0 <= x < 2^22 by 0 < d < 2^22 through a
-// float reciprocal: the product is within one unit of x/d, fixed by one step.
+// Exact quotient and remainder of 0 <= x < 2^22 by 0 < d < 2^22 through the
+// fp32 reciprocal r = RN(1/d), with no correction step and no branch: the
+// product p = RN((x + 1/2) r) (x + 1/2 is exact in fp32) is within a relative
+// 2^-23 of y = (x + 1/2) / d, i.e. within (x + 1/2) 2^-23 / d < 1 / (2d),
+// while y lies at least 1 / (2d) from every integer; so trunc(p) = floor(x/d).
 struct Div {
     float r;
     int d;
 };
+// r = 1.0f / d: fp32 division is correctly rounded, so r = RN(1/d).
 __device__ __forceinline__ Div mkdiv(int d) { return Div{1.0f / static_cast<float>(d), d}; }
 // The same from a reciprocal the plan rounded once to fp32 (FftDesc).
 __device__ __forceinline__ Div mkdiv(int d, float r) { return Div{r, d}; }
 __device__ __forceinline__ int qdiv(int x, Div v, int& rem) {
-    int q = static_cast<int>(static_cast<float>(x) * v.r);
-    int r = x - __mul24(q, v.d);
-    if (r < 0) { --q; r += v.d; }
-    else if (r >= v.d) { ++q; r -= v.d; }
-    rem = r;
+    const int q = static_cast<int>((static_cast<float>(x) + 0.5f) * v.r);
+    rem = x - __mul24(q, v.d);
     return q;
 }
 

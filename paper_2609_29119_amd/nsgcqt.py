@@ -120,12 +120,6 @@ def _check(status):
     return status
 
 
-def _stream(stream):
-    import torch
-    s = torch.cuda.current_stream() if stream is None else stream
-    return ctypes.c_void_p(s.cuda_stream)
-
-
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
@@ -161,6 +155,10 @@ class Plan:
         _check(L.nsgcqt_plan_info(self._h, ctypes.byref(self.info)))
         self.device = bool(self.info.device_tables)
         self._ws = {}
+        i = self.info
+        self._ws_need = {OP_ANALYSE: max(1, i.ws_analyse), OP_SYNTHESISE: max(1, i.ws_synthesise),
+                         OP_ADJ_ANALYSIS: max(1, i.ws_adjoint_analysis),
+                         OP_ADJ_SYNTHESIS: max(1, i.ws_adjoint_synthesis)}
 
     @classmethod
     def sliced(cls, fs, fmin, fmax, bins_per_octave, slice_len, slices_per_chunk=16, device=True):
@@ -232,16 +230,26 @@ class Plan:
         one if None), so the caching allocator ties it to the stream that
         uses it."""
         import torch
-        need = max(1, self.workspace_bytes(op))
         dev = torch.device(device or "cuda")
-        s = torch.cuda.current_stream(dev) if stream is None else stream
-        key = (op, s.cuda_stream)
-        ws = self._ws.get(key)
+        return self._ws_on(op, dev, torch.cuda.current_stream(dev) if stream is None else stream)
+
+    def _ws_on(self, op, dev, s):
+        ws = self._ws.get((op, s.cuda_stream))
+        need = self._ws_need[op]
         if ws is None or ws.numel() < need:
+            import torch
             with torch.cuda.stream(s):
                 ws = torch.empty(need, dtype=torch.uint8, device=dev)
-            self._ws[key] = ws
+            self._ws[(op, s.cuda_stream)] = ws
         return ws
+
+    @staticmethod
+    def _on(t, stream):
+        """The stream of a call on tensor t (t's device's current stream if
+        None) and its raw handle."""
+        import torch
+        s = torch.cuda.current_stream(t.device) if stream is None else stream
+        return s, ctypes.c_void_p(s.cuda_stream)
 
     def stage_info(self, op):
         """[(kernel name, algorithmic bytes per launch)] of one call of `op`."""
@@ -259,12 +267,13 @@ class Plan:
 
     def set_stage_events(self, handles):
         """Bracket kernel i of each call with handles[2i], handles[2i+1]
-        (see nsgcqt_set_stage_events); None stops."""
-        if not handles:
+        (see nsgcqt_set_stage_events); None stops. `handles` is a sequence
+        of event handles (None entries allowed) or a ctypes c_void_p array."""
+        if handles is None or len(handles) == 0:
             _check(lib().nsgcqt_set_stage_events(self._h, None, 0))
             return
-        arr = (ctypes.c_void_p * len(handles))(*handles)
-        _check(lib().nsgcqt_set_stage_events(self._h, arr, len(handles)))
+        arr = handles if isinstance(handles, ctypes.Array) else (ctypes.c_void_p * len(handles))(*handles)
+        _check(lib().nsgcqt_set_stage_events(self._h, arr, len(arr)))
 
     # ---------------------------------------------------------------- compute
     def _new(self, shape, dtype, like):
@@ -277,8 +286,9 @@ class Plan:
         self._expect(x, torch.float32, (self.batch, self.n_samples))
         out = self._new((self.batch, self.n_coeffs), torch.complex64, x) if out is None else out
         self._expect(out, torch.complex64, (self.batch, self.n_coeffs))
-        ws = self.workspace(OP_ANALYSE, x.device, stream) if ws is None else ws
-        _check(lib().nsgcqt_analyse(self._h, _ptr(x), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+        st, sh = self._on(x, stream)
+        ws = self._ws_on(OP_ANALYSE, x.device, st) if ws is None else ws
+        _check(lib().nsgcqt_analyse(self._h, _ptr(x), _ptr(out), _ptr(ws), ws.numel(), sh))
         return out
 
     def analyse_noalloc(self, x, out, stream=None):
@@ -287,7 +297,7 @@ class Plan:
         import torch
         self._expect(x, torch.float32, (self.batch, self.n_samples))
         self._expect(out, torch.complex64, (self.batch, self.n_coeffs))
-        _check(lib().nsgcqt_analyse_noalloc(self._h, _ptr(x), _ptr(out), _stream(stream)))
+        _check(lib().nsgcqt_analyse_noalloc(self._h, _ptr(x), _ptr(out), self._on(x, stream)[1]))
         return out
 
     def synthesise(self, c, out=None, ws=None, stream=None):
@@ -296,8 +306,9 @@ class Plan:
         self._expect(c, torch.complex64, (self.batch, self.n_coeffs))
         out = self._new((self.batch, self.n_samples), torch.float32, c) if out is None else out
         self._expect(out, torch.float32, (self.batch, self.n_samples))
-        ws = self.workspace(OP_SYNTHESISE, c.device, stream) if ws is None else ws
-        _check(lib().nsgcqt_synthesise(self._h, _ptr(c), _ptr(out), _ptr(ws), ws.numel(), _stream(stream)))
+        st, sh = self._on(c, stream)
+        ws = self._ws_on(OP_SYNTHESISE, c.device, st) if ws is None else ws
+        _check(lib().nsgcqt_synthesise(self._h, _ptr(c), _ptr(out), _ptr(ws), ws.numel(), sh))
         return out
 
     def adjoint(self, op, inp, out=None, ws=None, stream=None):
@@ -313,9 +324,9 @@ class Plan:
             raise ValueError("op must be OP_ADJ_ANALYSIS or OP_ADJ_SYNTHESIS")
         out = self._new(shape, dt, inp) if out is None else out
         self._expect(out, dt, shape)
-        ws = self.workspace(op, inp.device, stream) if ws is None else ws
-        _check(lib().nsgcqt_adjoint(self._h, int(op), _ptr(inp), _ptr(out), _ptr(ws), ws.numel(),
-                                    _stream(stream)))
+        st, sh = self._on(inp, stream)
+        ws = self._ws_on(op, inp.device, st) if ws is None else ws
+        _check(lib().nsgcqt_adjoint(self._h, int(op), _ptr(inp), _ptr(out), _ptr(ws), ws.numel(), sh))
         return out
 
     def slice_count(self, n):
@@ -332,9 +343,9 @@ class Plan:
         self._expect(x, torch.float32, (n,))
         out = self._new((J, self.n_coeffs), torch.complex64, x) if out is None else out
         self._expect(out, torch.complex64, (J, self.n_coeffs))
-        ws = self.workspace(OP_ANALYSE, x.device, stream) if ws is None else ws
-        _check(lib().nsgcqt_sliced_analyse(self._h, _ptr(x), n, _ptr(out), _ptr(ws), ws.numel(),
-                                           _stream(stream)))
+        st, sh = self._on(x, stream)
+        ws = self._ws_on(OP_ANALYSE, x.device, st) if ws is None else ws
+        _check(lib().nsgcqt_sliced_analyse(self._h, _ptr(x), n, _ptr(out), _ptr(ws), ws.numel(), sh))
         return out
 
     def sliced_synthesise(self, c, n, out=None, ws=None, stream=None):
@@ -344,9 +355,9 @@ class Plan:
         self._expect(c, torch.complex64, (J, self.n_coeffs))
         out = self._new((n,), torch.float32, c) if out is None else out
         self._expect(out, torch.float32, (n,))
-        ws = self.workspace(OP_SYNTHESISE, c.device, stream) if ws is None else ws
-        _check(lib().nsgcqt_sliced_synthesise(self._h, _ptr(c), int(n), _ptr(out), _ptr(ws), ws.numel(),
-                                              _stream(stream)))
+        st, sh = self._on(c, stream)
+        ws = self._ws_on(OP_SYNTHESISE, c.device, st) if ws is None else ws
+        _check(lib().nsgcqt_sliced_synthesise(self._h, _ptr(c), int(n), _ptr(out), _ptr(ws), ws.numel(), sh))
         return out
 
     @staticmethod
